@@ -1,0 +1,2 @@
+"""fp64 CPU oracle (test infrastructure only; never imported by the product path)."""
+from .sparvar_oracle import *  # noqa: F401,F403
