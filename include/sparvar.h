@@ -1,0 +1,210 @@
+/*
+ * sparvar.h -- C ABI of the SparVAR block-sparse cross-scale attention library
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * The library implements the sparse hot path of SparVAR (arXiv 2602.04361):
+ * queries of scale k of a next-scale-prediction VAR model attend to the
+ * concatenated key/value cache of scales 1..k (Sec. 3.1, Eq. (1)), restricted
+ * to kept b x b blocks: sink blocks on the early scales, a pattern selected at
+ * a decision scale S and carried to scale k by the cross-scale index mapping
+ * (Sec. 3.2 and the appendix "Cross-Scale Sparse Index Mapping"), and
+ * cross-scale local windows (Sec. 3.3).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - Scales are 1-based, as in the paper. The geometry struct is host memory
+ *    read during the call only.
+ *  - Tensors are [B, H, rows, d] with d contiguous and rows contiguous inside a
+ *    (batch, head) plane; consecutive planes (b-major, then h) are
+ *    `*_bh_stride` elements apart (>= rows * d), so a prefix of a preallocated
+ *    cache, or a slice of one scale's queries out of it, is passed without a
+ *    copy. Output tensors (o, lse, scores) are fully contiguous.
+ *  - Cache tokens are concatenated in scale order; inside a scale they are
+ *    row-major, token (x, y) of scale l at index C_{l-1} + x * w_l + y, where
+ *    C_l = N_1 + ... + N_l (appendix, Decompose step).
+ *  - Blocks are b x b spatial tiles of each scale; along an axis where the
+ *    scale is shorter than b the whole axis is one tile. Block ids run
+ *    scale-major and row-major over tiles inside a scale. Query tiles of
+ *    scale k use the same tiling ("query blocks" of the paper).
+ *  - Every pointer except the geometry is device memory owned by the caller.
+ *    The library allocates no device memory, keeps no global state and never
+ *    synchronises: work is enqueued on `stream` (NULL = the default stream)
+ *    and results are valid once the caller has synchronised that stream.
+ *  - Every call validates its arguments on the host before enqueueing any
+ *    work; on error nothing is written. Device data (index lists, block ids)
+ *    is not read on the host; kernels skip block ids that are out of range.
+ *  - Inputs must be finite. Outputs are bitwise deterministic for fixed
+ *    inputs and launch arguments.
+ *  - Supported: d in {64, 128}; dtype bf16 (bf16 MFMA, fp32 softmax and
+ *    accumulation, bf16 output rounded to nearest even) or fp32 (fp32 MFMA).
+ *  - Limits: 1 <= num_scales <= SPARVAR_MAX_SCALES, 1 <= block_edge <= 64,
+ *    total cache tokens < 2^31, B * H * rows < 2^31.
+ *
+ * Return value: SPARVAR_OK (0) or a negative status; a message for the last
+ * failure on the calling thread is available from sparvar_last_error().
+ */
+#ifndef SPARVAR_H_
+#define SPARVAR_H_
+
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SPARVAR_MAX_SCALES 32
+
+enum sparvar_status {
+  SPARVAR_OK = 0,
+  SPARVAR_ERR_INVALID = -1,     /* null pointer, bad shape, S >= k, topk <= 0, ... */
+  SPARVAR_ERR_UNSUPPORTED = -2, /* dtype or head dimension not supported */
+  SPARVAR_ERR_CAPACITY = -3,    /* output index buffer too small */
+  SPARVAR_ERR_HIP = -4          /* a HIP launch or runtime call failed */
+};
+
+typedef enum sparvar_dtype { SPARVAR_BF16 = 0, SPARVAR_F32 = 1 } sparvar_dtype_t;
+
+/* Scale schedule and tiling. h[l-1], w[l-1] are the rows and columns of scale
+ * l; the first num_sink_scales scales are the attention sink (appendix,
+ * Attention Sink paragraph). */
+typedef struct sparvar_geometry {
+  int32_t num_scales;
+  const int32_t* h;
+  const int32_t* w;
+  int32_t block_edge;
+  int32_t num_sink_scales;
+} sparvar_geometry_t;
+
+/* Derived geometry of one scale (host-only query). */
+typedef struct sparvar_scale_info {
+  int32_t h, w;            /* rows, columns */
+  int32_t n_tokens;        /* N_l = h * w */
+  int32_t token_offset;    /* C_{l-1}: first cache index of the scale */
+  int32_t n_tokens_le;     /* C_l = N_<=l: cache length at step l */
+  int32_t tile_h, tile_w;  /* tile edge e_h, e_w */
+  int32_t tiles_h, tiles_w;/* tiles per axis T_h, T_w; query tiles G_l = T_h * T_w */
+  int32_t block_offset;    /* id of the scale's first block */
+  int32_t n_blocks_le;     /* blocks in scales 1..l */
+} sparvar_scale_info_t;
+
+/* Fill *out for scale l (1-based) of geometry g. Host only, no GPU work. */
+int sparvar_scale_info(const sparvar_geometry_t* g, int32_t l, sparvar_scale_info_t* out);
+
+/*
+ * Dense cross-scale attention, Sec. 3.1 Eq. (1):
+ *   O[b,h,i,:] = sum_j softmax_j(softmax_scale * <Q[b,h,i,:], K[b,h,j,:]>) V[b,h,j,:]
+ * over all n_kv keys. q: [B,H,n_q,d] (plane stride q_bh_stride); k, v:
+ * [B,H,n_kv,d] (plane stride kv_bh_stride); o: [B,H,n_q,d] contiguous, same
+ * dtype as q. lse (nullable): [B,H,n_q] fp32, natural log of the softmax
+ * denominator of the scaled scores. Used at the decision scale (Sec. 3.2,
+ * dense attention at S) and as the dense baseline at every scale.
+ */
+int sparvar_dense_attn_fwd(int32_t B, int32_t H, int32_t n_q, int32_t n_kv, int32_t d,
+                           sparvar_dtype_t dtype, const void* q, int64_t q_bh_stride,
+                           const void* k, const void* v, int64_t kv_bh_stride, void* o,
+                           float* lse, float softmax_scale, hipStream_t stream);
+
+/*
+ * Decision-scale block selection, Sec. 3.2 (column-sum D and TopK) and the
+ * appendix "Hardware-Efficient Sparse Computation".
+ * Scores: P = softmax(softmax_scale * Q_S K_<=S^T) using lse_S from
+ * sparvar_dense_attn_fwd at scale S; score[b,h,g,v] = sum of P over the
+ * queries of query tile g of scale S and the keys of block v < NB_<=S.
+ * Selection: per row (b,h,g), the min(topk, NB_<=S) highest scores, ties to
+ * the lower block id, written ascending to topk_idx[b,h,g,0..topk) and padded
+ * with -1.
+ *   q_S: [B,H,N_S,d] (plane stride q_bh_stride); k_leS: [B,H,N_<=S,d] (plane
+ *   stride k_bh_stride); lse_S: [B,H,N_S] fp32.
+ *   scores_in (nullable): if set, selection runs on these fp32
+ *   [B,H,G_S,NB_<=S] scores and q_S, k_leS, lse_S are ignored (may be NULL).
+ *   scores_out (nullable): receives the computed scores; required when
+ *   scores_in is NULL.
+ *   topk_idx: int32 [B,H,G_S,topk]. 1 <= topk <= 1024.
+ */
+int sparvar_select_blocks(const sparvar_geometry_t* g, int32_t S, int32_t B, int32_t H,
+                          int32_t d, sparvar_dtype_t dtype, const void* q_S,
+                          int64_t q_bh_stride, const void* k_leS, int64_t k_bh_stride,
+                          const float* lse_S, float softmax_scale, const float* scores_in,
+                          float* scores_out, int32_t topk, int32_t* topk_idx,
+                          hipStream_t stream);
+
+/*
+ * Sink + cross-scale local blocks of every query tile of scale k (block form
+ * of the CSLA mask, Sec. 3.3, and the sink set of the appendix). Row g
+ * (query tile (a,c) = (g / T_w(k), g % T_w(k))) lists ascending:
+ *   - every block of scales 1..num_sink_scales;
+ *   - the scale-k tiles (a',c') with max(|a'-a|, |c'-c|) <= radius;
+ *   - the scale-(k-1) tiles overlapping the footprint of (a,c) rescaled to
+ *     scale k-1, widened by prev_dilation tiles per side.
+ * Head independent; compute once per (geometry, k, radius, dilation).
+ * row_ptr: int32 [G_k + 1]; col_idx: int32 [capacity], capacity >=
+ * sparvar_local_blocks_capacity(...). 1 <= k <= num_scales.
+ */
+int64_t sparvar_local_blocks_capacity(const sparvar_geometry_t* g, int32_t k, int32_t radius,
+                                      int32_t prev_dilation); /* exact nnz, < 0 on error */
+int sparvar_local_blocks(const sparvar_geometry_t* g, int32_t k, int32_t radius,
+                         int32_t prev_dilation, int32_t* row_ptr, int32_t* col_idx,
+                         int64_t capacity, hipStream_t stream);
+
+/*
+ * Cross-scale index mapping and merge into CSR (appendix "Cross-Scale Sparse
+ * Index Mapping" and "Attention Sink"). For target query tile (a,c) of scale
+ * k and every (b,h): the source tile is the Query Block Homography
+ * (floor((2a+1) T_h(S) / (2 T_h(k))), same for c); each selected block of
+ * topk_idx[b,h,source,:] (skipping -1) goes through Decompose-Align-Project:
+ * scale l -> l' = k - (S - l), tile origin (x,y) -> (floor(x h_l'/h_l),
+ * floor(y w_l'/w_l)), and the scale-l' tile containing it. The row is the
+ * ascending, duplicate-free union of the mapped blocks and local row (a,c).
+ * Row index r = (b*H + h) * G_k + g.
+ *   topk_idx: int32 [B,H,G_S,topk] (from sparvar_select_blocks).
+ *   local_row_ptr / local_col_idx: output of sparvar_local_blocks for k.
+ *   row_ptr: int32 [B*H*G_k + 1]; col_idx: int32 [capacity].
+ *   radius, prev_dilation: the values the local rows were built with; they
+ *   bound the local row length (longer local rows are cut to that bound).
+ *   capacity: >= sparvar_map_index_capacity(...) with the same arguments.
+ *   If the rows would overflow it anyway, rows are truncated so that nothing
+ *   is written beyond capacity.
+ *   schedule (nullable): int32 [B*H*G_k], the rows ordered longest first,
+ *   equal lengths in row order.
+ * Requires 1 <= S < k <= num_scales.
+ */
+int64_t sparvar_map_index_capacity(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t B,
+                                   int32_t H, int32_t topk, int32_t radius,
+                                   int32_t prev_dilation); /* upper bound, < 0 on error */
+int sparvar_map_index(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t B, int32_t H,
+                      int32_t topk, const int32_t* topk_idx, const int32_t* local_row_ptr,
+                      const int32_t* local_col_idx, int32_t radius, int32_t prev_dilation,
+                      int32_t* row_ptr, int32_t* col_idx, int64_t capacity, int32_t* schedule,
+                      hipStream_t stream);
+
+/*
+ * Block-sparse cross-scale attention at scale k (the sparse update
+ * Delta O of Sec. 3.2 and the block-masked attention of Sec. 3.3, Eq. (3)):
+ * every query of query tile g of (b,h) attends, with one softmax, to exactly
+ * the tokens of the blocks listed in CSR row r = (b*H + h) * G_k + g.
+ *   q_k: [B,H,N_k,d] (plane stride q_bh_stride); k_lek, v_lek: [B,H,N_<=k,d]
+ *   (plane stride kv_bh_stride); o: [B,H,N_k,d] contiguous; lse (nullable):
+ *   [B,H,N_k] fp32. A row with no valid block yields o = 0, lse = -inf.
+ *   row_ptr / col_idx: CSR over B*H*G_k rows with ascending block ids
+ *   (as written by sparvar_map_index); ids outside [0, NB_<=k) are skipped.
+ *   schedule (nullable): a permutation of the rows giving the launch order;
+ *   it changes only the order of work, never the results.
+ */
+int sparvar_block_sparse_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t B, int32_t H,
+                                  int32_t d, sparvar_dtype_t dtype, const void* q_k,
+                                  int64_t q_bh_stride, const void* k_lek, const void* v_lek,
+                                  int64_t kv_bh_stride, void* o, float* lse,
+                                  float softmax_scale, const int32_t* row_ptr,
+                                  const int32_t* col_idx, const int32_t* schedule,
+                                  hipStream_t stream);
+
+/* Static description of a status code. */
+const char* sparvar_status_string(int status);
+/* Message of the last failed call on this thread ("" if none). */
+const char* sparvar_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPARVAR_H_ */

@@ -1,0 +1,341 @@
+// C ABI entry points: host-side validation, geometry tables, launches.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+
+#include "geometry.h"
+#include "launch.h"
+#include "sparvar.h"
+
+using namespace sparvar;
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+int ok() {
+  g_last_error[0] = '\0';
+  return SPARVAR_OK;
+}
+
+int hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return ok();
+  return fail(SPARVAR_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Env knobs for launch shape experiments (defaults are the tuned choice).
+int env_int(const char* name, int dflt) {
+  const char* s = std::getenv(name);
+  return s ? std::atoi(s) : dflt;
+}
+
+int build_table(const sparvar_geometry_t* g, GeoTable* T) {
+  if (!g) return fail(SPARVAR_ERR_INVALID, "geometry is NULL");
+  if (g->num_scales < 1 || g->num_scales > kMaxScales)
+    return fail(SPARVAR_ERR_INVALID, "num_scales %d outside [1, %d]", g->num_scales, kMaxScales);
+  if (!g->h || !g->w) return fail(SPARVAR_ERR_INVALID, "geometry h/w is NULL");
+  if (g->block_edge < 1 || g->block_edge > 64)
+    return fail(SPARVAR_ERR_INVALID, "block_edge %d outside [1, 64]", g->block_edge);
+  if (g->num_sink_scales < 0) return fail(SPARVAR_ERR_INVALID, "num_sink_scales < 0");
+  std::memset(T, 0, sizeof(*T));
+  T->L = g->num_scales;
+  T->b = g->block_edge;
+  T->n_sink = g->num_sink_scales < g->num_scales ? g->num_sink_scales : g->num_scales;
+  int64_t tok = 0, blk = 0;
+  for (int i = 0; i < T->L; ++i) {
+    const int32_t h = g->h[i], w = g->w[i];
+    if (h < 1 || w < 1) return fail(SPARVAR_ERR_INVALID, "scale %d has size %dx%d", i + 1, h, w);
+    T->h[i] = h;
+    T->w[i] = w;
+    T->eh[i] = h < T->b ? h : T->b;
+    T->ew[i] = w < T->b ? w : T->b;
+    T->Th[i] = (h + T->eh[i] - 1) / T->eh[i];
+    T->Tw[i] = (w + T->ew[i] - 1) / T->ew[i];
+    tok += (int64_t)h * w;
+    blk += (int64_t)T->Th[i] * T->Tw[i];
+    if (tok >= (int64_t(1) << 31) || blk >= (int64_t(1) << 31))
+      return fail(SPARVAR_ERR_INVALID, "cache longer than 2^31 tokens");
+    T->C[i + 1] = (int32_t)tok;
+    T->NB[i + 1] = (int32_t)blk;
+  }
+  return SPARVAR_OK;
+}
+
+int check_dtype_d(sparvar_dtype_t dt, int32_t d) {
+  if (dt != SPARVAR_BF16 && dt != SPARVAR_F32) return fail(SPARVAR_ERR_UNSUPPORTED, "dtype %d not supported", (int)dt);
+  if (d != 64 && d != 128) return fail(SPARVAR_ERR_UNSUPPORTED, "head dim %d not supported (64 or 128)", d);
+  return SPARVAR_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+int check_plane(const void* p, int64_t stride, int64_t rows, int32_t d, int elem, const char* name) {
+  if (!p) return fail(SPARVAR_ERR_INVALID, "%s is NULL", name);
+  if (!aligned16(p)) return fail(SPARVAR_ERR_INVALID, "%s is not 16-byte aligned", name);
+  if (stride < rows * d) return fail(SPARVAR_ERR_INVALID, "%s plane stride %lld < rows*d = %lld", name,
+                                     (long long)stride, (long long)(rows * d));
+  if ((stride * elem) % 16 != 0) return fail(SPARVAR_ERR_INVALID, "%s plane stride is not a multiple of 16 bytes", name);
+  return SPARVAR_OK;
+}
+
+int32_t local_max_len(const GeoTable& T, int k, int32_t r, int32_t dil, int64_t* total) {
+  int32_t mx = 0;
+  int64_t sum = 0;
+  for (int32_t g = 0; g < tiles_of(T, k); ++g) {
+    const int32_t n = local_row_len(local_row(T, k, r, dil, g));
+    mx = n > mx ? n : mx;
+    sum += n;
+  }
+  if (total) *total = sum;
+  return mx;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sparvar_status_string(int status) {
+  switch (status) {
+    case SPARVAR_OK: return "ok";
+    case SPARVAR_ERR_INVALID: return "invalid argument";
+    case SPARVAR_ERR_UNSUPPORTED: return "unsupported dtype or head dimension";
+    case SPARVAR_ERR_CAPACITY: return "index capacity too small";
+    case SPARVAR_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* sparvar_last_error(void) { return g_last_error; }
+
+int sparvar_scale_info(const sparvar_geometry_t* g, int32_t l, sparvar_scale_info_t* out) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if (!out) return fail(SPARVAR_ERR_INVALID, "out is NULL");
+  if (l < 1 || l > T.L) return fail(SPARVAR_ERR_INVALID, "scale %d outside [1, %d]", l, T.L);
+  out->h = T.h[l - 1];
+  out->w = T.w[l - 1];
+  out->n_tokens = T.h[l - 1] * T.w[l - 1];
+  out->token_offset = T.C[l - 1];
+  out->n_tokens_le = T.C[l];
+  out->tile_h = T.eh[l - 1];
+  out->tile_w = T.ew[l - 1];
+  out->tiles_h = T.Th[l - 1];
+  out->tiles_w = T.Tw[l - 1];
+  out->block_offset = T.NB[l - 1];
+  out->n_blocks_le = T.NB[l];
+  return ok();
+}
+
+int sparvar_dense_attn_fwd(int32_t B, int32_t H, int32_t n_q, int32_t n_kv, int32_t d,
+                           sparvar_dtype_t dtype, const void* q, int64_t q_bh_stride,
+                           const void* k, const void* v, int64_t kv_bh_stride, void* o,
+                           float* lse, float softmax_scale, hipStream_t stream) {
+  int st = check_dtype_d(dtype, d);
+  if (st) return st;
+  if (B < 1 || H < 1 || n_q < 1 || n_kv < 1) return fail(SPARVAR_ERR_INVALID, "B, H, n_q, n_kv must be >= 1");
+  if ((int64_t)B * H * n_q >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "B*H*n_q too large");
+  if (!(std::isfinite(softmax_scale))) return fail(SPARVAR_ERR_INVALID, "softmax_scale is not finite");
+  const int elem = dtype == SPARVAR_BF16 ? 2 : 4;
+  if ((st = check_plane(q, q_bh_stride, n_q, d, elem, "q"))) return st;
+  if ((st = check_plane(k, kv_bh_stride, n_kv, d, elem, "k"))) return st;
+  if ((st = check_plane(v, kv_bh_stride, n_kv, d, elem, "v"))) return st;
+  if ((st = check_plane(o, (int64_t)n_q * d, n_q, d, elem, "o"))) return st;
+  DenseAttnArgs a;
+  a.BH = B * H;
+  a.n_q = n_q;
+  a.n_kv = n_kv;
+  a.d = d;
+  a.bf16 = dtype == SPARVAR_BF16;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.o = o;
+  a.lse = lse;
+  a.q_bh_stride = q_bh_stride;
+  a.kv_bh_stride = kv_bh_stride;
+  a.softmax_scale = softmax_scale;
+  a.waves = env_int("SPARVAR_DENSE_WAVES", 0);
+  a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
+  return hip_status(launch_dense_attn(a, stream), "dense attention launch");
+}
+
+int sparvar_select_blocks(const sparvar_geometry_t* g, int32_t S, int32_t B, int32_t H,
+                          int32_t d, sparvar_dtype_t dtype, const void* q_S,
+                          int64_t q_bh_stride, const void* k_leS, int64_t k_bh_stride,
+                          const float* lse_S, float softmax_scale, const float* scores_in,
+                          float* scores_out, int32_t topk, int32_t* topk_idx,
+                          hipStream_t stream) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if (S < 1 || S > T.L) return fail(SPARVAR_ERR_INVALID, "decision scale %d outside [1, %d]", S, T.L);
+  if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
+  if (topk < 1 || topk > 1024) return fail(SPARVAR_ERR_INVALID, "topk %d outside [1, 1024]", topk);
+  if (!topk_idx) return fail(SPARVAR_ERR_INVALID, "topk_idx is NULL");
+  const int32_t NB = T.NB[S];
+  if ((int64_t)NB * 8 > 64 * 1024) return fail(SPARVAR_ERR_UNSUPPORTED, "%d candidate blocks exceed the selection kernel's LDS", NB);
+  const int64_t rows = (int64_t)B * H * tiles_of(T, S);
+  if (rows * (NB > topk ? NB : topk) >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "score tensor too large");
+  const float* sel_in = scores_in;
+  if (!scores_in) {
+    if (!scores_out) return fail(SPARVAR_ERR_INVALID, "scores_out is required when scores_in is NULL");
+    if ((st = check_dtype_d(dtype, d))) return st;
+    if (T.eh[S - 1] * T.ew[S - 1] > 256)
+      return fail(SPARVAR_ERR_UNSUPPORTED, "query tiles above 256 tokens are not supported by the scoring kernel");
+    if (!lse_S) return fail(SPARVAR_ERR_INVALID, "lse_S is NULL");
+    if (!(std::isfinite(softmax_scale))) return fail(SPARVAR_ERR_INVALID, "softmax_scale is not finite");
+    const int elem = dtype == SPARVAR_BF16 ? 2 : 4;
+    const int32_t NS = T.h[S - 1] * T.w[S - 1];
+    if ((st = check_plane(q_S, q_bh_stride, NS, d, elem, "q_S"))) return st;
+    if ((st = check_plane(k_leS, k_bh_stride, T.C[S], d, elem, "k_leS"))) return st;
+    ScoreArgs a;
+    a.G = &T;
+    a.S = S;
+    a.BH = B * H;
+    a.d = d;
+    a.bf16 = dtype == SPARVAR_BF16;
+    a.q = q_S;
+    a.k = k_leS;
+    a.q_bh_stride = q_bh_stride;
+    a.k_bh_stride = k_bh_stride;
+    a.lse = lse_S;
+    a.softmax_scale = softmax_scale;
+    a.scores = scores_out;
+    hipError_t e = launch_pooled_scores(a, stream);
+    if (e != hipSuccess) return hip_status(e, "pooled score launch");
+    sel_in = scores_out;
+  }
+  return hip_status(launch_topk(sel_in, (int32_t)rows, NB, topk, topk_idx, stream), "top-k launch");
+}
+
+int64_t sparvar_local_blocks_capacity(const sparvar_geometry_t* g, int32_t k, int32_t radius,
+                                      int32_t prev_dilation) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if (k < 1 || k > T.L) return fail(SPARVAR_ERR_INVALID, "scale %d outside [1, %d]", k, T.L);
+  if (radius < 0 || prev_dilation < 0) return fail(SPARVAR_ERR_INVALID, "radius and dilation must be >= 0");
+  int64_t total = 0;
+  local_max_len(T, k, radius, prev_dilation, &total);
+  ok();
+  return total;
+}
+
+int sparvar_local_blocks(const sparvar_geometry_t* g, int32_t k, int32_t radius,
+                         int32_t prev_dilation, int32_t* row_ptr, int32_t* col_idx,
+                         int64_t capacity, hipStream_t stream) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if (k < 1 || k > T.L) return fail(SPARVAR_ERR_INVALID, "scale %d outside [1, %d]", k, T.L);
+  if (radius < 0 || prev_dilation < 0) return fail(SPARVAR_ERR_INVALID, "radius and dilation must be >= 0");
+  if (!row_ptr || !col_idx) return fail(SPARVAR_ERR_INVALID, "row_ptr/col_idx is NULL");
+  int64_t total = 0;
+  local_max_len(T, k, radius, prev_dilation, &total);
+  if (total >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "local lists too large");
+  if (capacity < total)
+    return fail(SPARVAR_ERR_CAPACITY, "capacity %lld < %lld entries", (long long)capacity, (long long)total);
+  return hip_status(launch_local_blocks(T, k, radius, prev_dilation, row_ptr, col_idx, stream), "local blocks launch");
+}
+
+int64_t sparvar_map_index_capacity(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t B,
+                                   int32_t H, int32_t topk, int32_t radius,
+                                   int32_t prev_dilation) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if (S < 1 || k > T.L || S >= k) return fail(SPARVAR_ERR_INVALID, "need 1 <= S < k <= %d (S=%d, k=%d)", T.L, S, k);
+  if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
+  if (topk < 1 || topk > 1024) return fail(SPARVAR_ERR_INVALID, "topk %d outside [1, 1024]", topk);
+  if (radius < 0 || prev_dilation < 0) return fail(SPARVAR_ERR_INVALID, "radius and dilation must be >= 0");
+  const int32_t mx = local_max_len(T, k, radius, prev_dilation, nullptr);
+  ok();
+  return (int64_t)B * H * tiles_of(T, k) * (int64_t)(mx + topk);
+}
+
+int sparvar_map_index(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t B, int32_t H,
+                      int32_t topk, const int32_t* topk_idx, const int32_t* local_row_ptr,
+                      const int32_t* local_col_idx, int32_t radius, int32_t prev_dilation,
+                      int32_t* row_ptr, int32_t* col_idx, int64_t capacity, int32_t* schedule,
+                      hipStream_t stream) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if (S < 1 || k > T.L || S >= k) return fail(SPARVAR_ERR_INVALID, "need 1 <= S < k <= %d (S=%d, k=%d)", T.L, S, k);
+  if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
+  if (topk < 1 || topk > 1024) return fail(SPARVAR_ERR_INVALID, "topk %d outside [1, 1024]", topk);
+  if (radius < 0 || prev_dilation < 0) return fail(SPARVAR_ERR_INVALID, "radius and dilation must be >= 0");
+  if (!topk_idx || !local_row_ptr || !local_col_idx || !row_ptr || !col_idx)
+    return fail(SPARVAR_ERR_INVALID, "a required pointer is NULL");
+  const int32_t mx = local_max_len(T, k, radius, prev_dilation, nullptr);
+  const int64_t rows = (int64_t)B * H * tiles_of(T, k);
+  const int64_t need = rows * (int64_t)(mx + topk);
+  if (rows >= (int64_t(1) << 31) || need >= (int64_t(1) << 31))
+    return fail(SPARVAR_ERR_INVALID, "index lists too large for int32 offsets");
+  if (capacity < need)
+    return fail(SPARVAR_ERR_CAPACITY, "capacity %lld < bound %lld", (long long)capacity, (long long)need);
+  if ((int64_t)(mx + topk) * 2 * 4 * 4 > 64 * 1024)
+    return fail(SPARVAR_ERR_UNSUPPORTED, "rows of %d candidates exceed the merge kernel's LDS", mx + topk);
+  return hip_status(launch_map_index(T, S, k, B * H, topk, topk_idx, local_row_ptr, local_col_idx, mx, row_ptr,
+                                     col_idx, capacity, schedule, stream),
+                    "map index launch");
+}
+
+int sparvar_block_sparse_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t B, int32_t H,
+                                  int32_t d, sparvar_dtype_t dtype, const void* q_k,
+                                  int64_t q_bh_stride, const void* k_lek, const void* v_lek,
+                                  int64_t kv_bh_stride, void* o, float* lse,
+                                  float softmax_scale, const int32_t* row_ptr,
+                                  const int32_t* col_idx, const int32_t* schedule,
+                                  hipStream_t stream) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if ((st = check_dtype_d(dtype, d))) return st;
+  if (k < 1 || k > T.L) return fail(SPARVAR_ERR_INVALID, "scale %d outside [1, %d]", k, T.L);
+  if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
+  if (!row_ptr || !col_idx) return fail(SPARVAR_ERR_INVALID, "row_ptr/col_idx is NULL");
+  if (!(std::isfinite(softmax_scale))) return fail(SPARVAR_ERR_INVALID, "softmax_scale is not finite");
+  const int32_t Nk = T.h[k - 1] * T.w[k - 1];
+  if ((int64_t)B * H * Nk >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "B*H*N_k too large");
+  const int elem = dtype == SPARVAR_BF16 ? 2 : 4;
+  if ((st = check_plane(q_k, q_bh_stride, Nk, d, elem, "q_k"))) return st;
+  if ((st = check_plane(k_lek, kv_bh_stride, T.C[k], d, elem, "k_lek"))) return st;
+  if ((st = check_plane(v_lek, kv_bh_stride, T.C[k], d, elem, "v_lek"))) return st;
+  if ((st = check_plane(o, (int64_t)Nk * d, Nk, d, elem, "o"))) return st;
+  SparseAttnArgs a;
+  a.G = &T;
+  a.k = k;
+  a.BH = B * H;
+  a.d = d;
+  a.bf16 = dtype == SPARVAR_BF16;
+  a.q = q_k;
+  a.k_cache = k_lek;
+  a.v_cache = v_lek;
+  a.o = o;
+  a.lse = lse;
+  a.q_bh_stride = q_bh_stride;
+  a.kv_bh_stride = kv_bh_stride;
+  a.softmax_scale = softmax_scale;
+  a.row_ptr = row_ptr;
+  a.col_idx = col_idx;
+  a.schedule = schedule;
+  a.waves = env_int("SPARVAR_SPARSE_WAVES", 0);
+  a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
+  return hip_status(launch_sparse_attn(a, stream), "block-sparse attention launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,157 @@
+// Device-side building blocks shared by the attention and scoring kernels:
+// MFMA fragment types, key chunks, and the S^T = K Q^T tile product.
+//
+// Layout choice (CDNA MFMA 32x32): the score tile is computed transposed,
+// S^T[key][query] = K Q^T, so that a lane owns one query column and 16 keys.
+// Row-wise softmax statistics are then lane-local plus one exchange between
+// the two 32-lane halves, and the probabilities leave the accumulator already
+// in the B-operand layout of the P V^T product (O^T = V^T P^T).
+//
+// Accumulator layout of a 32x32 MFMA tile: register r of lane
+// (col = lane % 32, half = lane / 32) holds row 8 * (r / 4) + 4 * half + r % 4.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "geometry.h"
+
+namespace sparvar {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+typedef uint16_t bf16_bits;
+
+constexpr int kChunk = 64;     // keys per chunk
+constexpr int kQPerWave = 32;  // queries per wave (MFMA N)
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// Keys of a chunk: slot s < count is token base + (s / nc) * stride + s % nc.
+struct Chunk {
+  int32_t base, nc, stride, count, magic;  // magic = ceil(65536 / nc): s / nc == (s * magic) >> 16 for s < 64
+};
+
+__device__ __forceinline__ int32_t chunk_token(const Chunk& c, int32_t s) {
+  const int32_t q = (s * c.magic) >> 16;
+  return c.base + q * c.stride + (s - q * c.nc);
+}
+
+__device__ __forceinline__ int32_t div_magic(int32_t nc) { return (65536 + nc - 1) / nc; }
+
+__device__ __forceinline__ Chunk make_chunk(int32_t base, int32_t nc, int32_t stride, int32_t count) {
+  Chunk c;
+  c.base = base;
+  c.nc = nc;
+  c.stride = stride;
+  c.count = count;
+  c.magic = div_magic(nc);
+  return c;
+}
+
+// Contiguous run of count tokens starting at base.
+__device__ __forceinline__ Chunk run_chunk(int32_t base, int32_t count) {
+  return make_chunk(base, kChunk, kChunk, count);
+}
+
+__device__ __forceinline__ u32x4 ldg16(const void* p) {
+  return *reinterpret_cast<const u32x4*>(p);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+__device__ __forceinline__ f32x16 mfma_bf16(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x16 mfma_f32(float a, float b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x16 zero16() {
+  f32x16 z;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) z[i] = 0.f;
+  return z;
+}
+
+// Round to nearest even fp32 -> bf16 (hardware conversion on gfx950).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+  bf16x2 v;
+  v[0] = (__bf16)lo;
+  v[1] = (__bf16)hi;
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+__device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32, 64); }
+
+// Query fragments (B operand of S^T = K Q^T) for the lane's query row.
+// bf16: step s holds d in [16 s + 8 half, +8). fp32: step s holds d = 2 s + half.
+template <int D>
+struct QFragBF16 {
+  bf16x8 f[D / 16];
+  __device__ __forceinline__ void load(const bf16_bits* row, int half) {
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) f[s] = as_bf16x8(ldg16(row + 16 * s + 8 * half));
+  }
+};
+
+template <int D>
+struct QFragF32 {
+  float f[D / 2];
+  __device__ __forceinline__ void load(const float* row, int half) {
+#pragma unroll
+    for (int s = 0; s < D / 2; ++s) f[s] = row[2 * s + half];
+  }
+};
+
+// S^T for one 64-key chunk and the wave's 32 queries: st[kt] covers keys
+// 32 kt .. 32 kt + 31 (rows) x 32 queries (columns). Key slots past the chunk's
+// count load a valid token (slot 0) and must be masked by the caller.
+template <int D>
+__device__ __forceinline__ void chunk_scores(const bf16_bits* kplane, const Chunk& c,
+                                             const QFragBF16<D>& q, int l32, int half,
+                                             f32x16 st[2]) {
+  const bf16_bits* krow[2];
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt) {
+    const int32_t s = 32 * kt + l32;
+    krow[kt] = kplane + (int64_t)chunk_token(c, s < c.count ? s : 0) * D + 8 * half;
+    st[kt] = zero16();
+  }
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) {
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) st[kt] = mfma_bf16(as_bf16x8(ldg16(krow[kt] + 16 * s)), q.f[s], st[kt]);
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void chunk_scores(const float* kplane, const Chunk& c,
+                                             const QFragF32<D>& q, int l32, int half,
+                                             f32x16 st[2]) {
+  const float* krow[2];
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt) {
+    const int32_t s = 32 * kt + l32;
+    krow[kt] = kplane + (int64_t)chunk_token(c, s < c.count ? s : 0) * D + half;
+    st[kt] = zero16();
+  }
+#pragma unroll
+  for (int s = 0; s < D / 2; ++s) {
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) st[kt] = mfma_f32(krow[kt][2 * s], q.f[s], st[kt]);
+  }
+}
+
+// Key index (within the chunk) of accumulator register r of key tile kt.
+__device__ __forceinline__ int key_of(int kt, int r, int half) {
+  return 32 * kt + 8 * (r >> 2) + 4 * half + (r & 3);
+}
+
+// Uniform (wave-invariant) value hint.
+__device__ __forceinline__ int32_t uniform(int32_t x) { return __builtin_amdgcn_readfirstlane(x); }
+
+}  // namespace sparvar

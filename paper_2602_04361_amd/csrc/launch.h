@@ -1,0 +1,60 @@
+// Internal launchers called by the C ABI after host-side validation.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "geometry.h"
+
+namespace sparvar {
+
+struct DenseAttnArgs {
+  int32_t BH, n_q, n_kv, d;
+  bool bf16;
+  const void *q, *k, *v;
+  void* o;
+  float* lse;
+  int64_t q_bh_stride, kv_bh_stride;
+  float softmax_scale;
+  int waves;    // 0 = default
+  int swizzle;  // XCD-aware workgroup order
+};
+
+struct SparseAttnArgs {
+  const GeoTable* G;
+  int32_t k, BH, d;
+  bool bf16;
+  const void *q, *k_cache, *v_cache;
+  void* o;
+  float* lse;
+  int64_t q_bh_stride, kv_bh_stride;
+  float softmax_scale;
+  const int32_t *row_ptr, *col_idx, *schedule;
+  int waves;    // 0 = from the tile size
+  int swizzle;
+};
+
+struct ScoreArgs {
+  const GeoTable* G;
+  int32_t S, BH, d;
+  bool bf16;
+  const void *q, *k;
+  int64_t q_bh_stride, k_bh_stride;
+  const float* lse;
+  float softmax_scale;
+  float* scores;
+};
+
+hipError_t launch_dense_attn(const DenseAttnArgs& a, hipStream_t stream);
+hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream);
+hipError_t launch_pooled_scores(const ScoreArgs& a, hipStream_t stream);
+hipError_t launch_topk(const float* scores, int32_t rows, int32_t nb, int32_t topk, int32_t* out,
+                       hipStream_t stream);
+hipError_t launch_local_blocks(const GeoTable& G, int k, int32_t radius, int32_t dil, int32_t* row_ptr,
+                               int32_t* col_idx, hipStream_t stream);
+hipError_t launch_map_index(const GeoTable& G, int S, int k, int32_t BH, int32_t topk,
+                            const int32_t* topk_idx, const int32_t* local_row_ptr,
+                            const int32_t* local_col_idx, int32_t max_local, int32_t* row_ptr,
+                            int32_t* col_idx, int64_t capacity, int32_t* schedule, hipStream_t stream);
+
+}  // namespace sparvar

@@ -1,0 +1,92 @@
+"""One layer of the SparVAR sparse path on the GPU, as a sequence of C-ABI calls.
+
+SparsePath owns the device buffers (allocated with torch) and issues, on the
+current stream:
+  decision(): dense attention with LSE at the decision scale S, then pooled
+              block scores and per-query-tile top-k (sparvar_select_blocks);
+  step(k):    sparvar_map_index (mapped + local blocks -> CSR + schedule), then
+              sparvar_block_sparse_attn_fwd at scale k.
+Local rows are geometry-only and built once per step by build_local().
+All arithmetic runs in libsparvar.so; this module only allocates and calls.
+"""
+from __future__ import annotations
+
+import math
+
+import torch
+
+from . import sparvar as sv
+
+
+class SparsePath:
+    def __init__(self, geom: sv.Geometry, S, steps, B, H, d, topk, radius, prev_dilation=0,
+                 dtype=torch.bfloat16, device="cuda", use_schedule=True, softmax_scale=None):
+        self.g = geom
+        self.S, self.steps = int(S), [int(k) for k in steps]
+        self.B, self.H, self.d = B, H, d
+        self.topk, self.radius, self.dil = topk, radius, prev_dilation
+        self.dtype, self.device = dtype, device
+        self.scale = float(torch.tensor(1.0 / math.sqrt(d), dtype=torch.float32)) if softmax_scale is None \
+            else float(softmax_scale)
+        info = {l: geom.scale_info(l) for l in range(1, len(geom.h) + 1)}
+        self.info = info
+        iS = info[S]
+        G_S, NB_S = iS["tiles_h"] * iS["tiles_w"], iS["n_blocks_le"]
+        i32 = dict(dtype=torch.int32, device=device)
+        self.o_S = torch.empty(B, H, iS["n_tokens"], d, dtype=dtype, device=device)
+        self.lse_S = torch.empty(B, H, iS["n_tokens"], dtype=torch.float32, device=device)
+        self.scores = torch.empty(B, H, G_S, NB_S, dtype=torch.float32, device=device)
+        self.topk_idx = torch.empty(B, H, G_S, topk, **i32)
+        self.local, self.csr, self.out = {}, {}, {}
+        for k in self.steps:
+            ik = info[k]
+            G_k = ik["tiles_h"] * ik["tiles_w"]
+            cap_l = sv.sparvar_local_blocks_capacity(geom, k, radius, prev_dilation)
+            self.local[k] = (torch.empty(G_k + 1, **i32), torch.empty(max(cap_l, 1), **i32))
+            cap = sv.sparvar_map_index_capacity(geom, S, k, B, H, topk, radius, prev_dilation)
+            rows = B * H * G_k
+            self.csr[k] = (torch.empty(rows + 1, **i32), torch.empty(cap, **i32),
+                           torch.empty(rows, **i32) if use_schedule else None)
+            self.out[k] = torch.empty(B, H, ik["n_tokens"], d, dtype=dtype, device=device)
+
+    # ------------------------------------------------------------------ calls
+    def build_local(self):
+        for k in self.steps:
+            rp, ci = self.local[k]
+            sv.sparvar_local_blocks(self.g, k, self.radius, rp, ci, prev_dilation=self.dil)
+
+    def q_slice(self, Q_all, l):
+        i = self.info[l]
+        return Q_all[:, :, i["token_offset"]:i["n_tokens_le"]]
+
+    def kv_prefix(self, X_all, l):
+        return X_all[:, :, :self.info[l]["n_tokens_le"]]
+
+    def decision(self, Q_all, K_all, V_all):
+        S = self.S
+        q, kk, vv = self.q_slice(Q_all, S), self.kv_prefix(K_all, S), self.kv_prefix(V_all, S)
+        sv.sparvar_dense_attn_fwd(q, kk, vv, self.o_S, self.lse_S, softmax_scale=self.scale)
+        sv.sparvar_select_blocks(self.g, S, q, kk, self.lse_S, self.topk, self.topk_idx, scores_out=self.scores,
+                                 softmax_scale=self.scale)
+
+    def map_step(self, k):
+        rp_l, ci_l = self.local[k]
+        rp, ci, sch = self.csr[k]
+        sv.sparvar_map_index(self.g, self.S, k, self.B, self.H, self.topk, self.topk_idx, rp_l, ci_l, self.radius,
+                             rp, ci, schedule=sch, prev_dilation=self.dil)
+
+    def attn_step(self, k, Q_all, K_all, V_all, lse=None, use_schedule=True):
+        rp, ci, sch = self.csr[k]
+        sv.sparvar_block_sparse_attn_fwd(self.g, k, self.q_slice(Q_all, k), self.kv_prefix(K_all, k),
+                                         self.kv_prefix(V_all, k), self.out[k], rp, ci, lse=lse,
+                                         schedule=sch if use_schedule else None, softmax_scale=self.scale)
+
+    def step(self, k, Q_all, K_all, V_all):
+        self.map_step(k)
+        self.attn_step(k, Q_all, K_all, V_all)
+
+    def run(self, Q_all, K_all, V_all):
+        """Decision step plus every sparse step (local rows must be built)."""
+        self.decision(Q_all, K_all, V_all)
+        for k in self.steps:
+            self.step(k, Q_all, K_all, V_all)

@@ -1,0 +1,236 @@
+"""ctypes binding of libsparvar.so (argument marshalling only).
+
+Every function here has the name of the C entry point it calls and forwards
+torch tensors as raw device pointers, plane strides and the current HIP stream.
+No computation happens in Python. If the shared library is missing the first
+call raises: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libsparvar.so")
+
+OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_CAPACITY, ERR_HIP = 0, -1, -2, -3, -4
+BF16, F32 = 0, 1
+MAX_SCALES = 32
+
+EXPORTS = [
+    "sparvar_scale_info",
+    "sparvar_dense_attn_fwd",
+    "sparvar_select_blocks",
+    "sparvar_local_blocks_capacity",
+    "sparvar_local_blocks",
+    "sparvar_map_index_capacity",
+    "sparvar_map_index",
+    "sparvar_block_sparse_attn_fwd",
+    "sparvar_status_string",
+    "sparvar_last_error",
+]
+
+
+class SparvarError(RuntimeError):
+    def __init__(self, status, message):
+        super().__init__(f"{message} (status {status})")
+        self.status = status
+
+
+class _CGeometry(ctypes.Structure):
+    _fields_ = [
+        ("num_scales", ctypes.c_int32),
+        ("h", ctypes.POINTER(ctypes.c_int32)),
+        ("w", ctypes.POINTER(ctypes.c_int32)),
+        ("block_edge", ctypes.c_int32),
+        ("num_sink_scales", ctypes.c_int32),
+    ]
+
+
+class _CScaleInfo(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "h", "w", "n_tokens", "token_offset", "n_tokens_le", "tile_h", "tile_w",
+        "tiles_h", "tiles_w", "block_offset", "n_blocks_le")]
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libsparvar.so once and declare the C signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is missing: build it with `python -m paper_2602_04361_amd.build`")
+    lib = ctypes.CDLL(path)
+    i32, i64, f32, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
+    G = ctypes.POINTER(_CGeometry)
+    sig = {
+        "sparvar_scale_info": (ctypes.c_int, [G, i32, ctypes.POINTER(_CScaleInfo)]),
+        "sparvar_dense_attn_fwd": (ctypes.c_int, [i32, i32, i32, i32, i32, ctypes.c_int, vp, i64, vp, vp, i64, vp,
+                                                  vp, f32, vp]),
+        "sparvar_select_blocks": (ctypes.c_int, [G, i32, i32, i32, i32, ctypes.c_int, vp, i64, vp, i64, vp, f32, vp,
+                                                 vp, i32, vp, vp]),
+        "sparvar_local_blocks_capacity": (i64, [G, i32, i32, i32]),
+        "sparvar_local_blocks": (ctypes.c_int, [G, i32, i32, i32, vp, vp, i64, vp]),
+        "sparvar_map_index_capacity": (i64, [G, i32, i32, i32, i32, i32, i32, i32]),
+        "sparvar_map_index": (ctypes.c_int, [G, i32, i32, i32, i32, i32, vp, vp, vp, i32, i32, vp, vp, i64, vp, vp]),
+        "sparvar_block_sparse_attn_fwd": (ctypes.c_int, [G, i32, i32, i32, i32, ctypes.c_int, vp, i64, vp, vp, i64,
+                                                         vp, vp, f32, vp, vp, vp, vp]),
+        "sparvar_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "sparvar_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = lib
+    return lib
+
+
+def _check(status):
+    if status != OK:
+        lib = load_library()
+        raise SparvarError(status, lib.sparvar_last_error().decode() or lib.sparvar_status_string(status).decode())
+
+
+class Geometry:
+    """Host-side sparvar_geometry_t: scale sizes, block edge, sink scales."""
+
+    def __init__(self, h, w, block_edge, num_sink_scales):
+        self.h = [int(x) for x in h]
+        self.w = [int(x) for x in w]
+        self.block_edge = int(block_edge)
+        self.num_sink_scales = int(num_sink_scales)
+        n = len(self.h)
+        self._h = (ctypes.c_int32 * n)(*self.h)
+        self._w = (ctypes.c_int32 * n)(*self.w)
+        self.c = _CGeometry(n, self._h, self._w, self.block_edge, self.num_sink_scales)
+
+    @property
+    def ref(self):
+        return ctypes.byref(self.c)
+
+    def scale_info(self, l):
+        info = _CScaleInfo()
+        _check(load_library().sparvar_scale_info(self.ref, int(l), ctypes.byref(info)))
+        return {n: getattr(info, n) for n, _ in _CScaleInfo._fields_}
+
+
+# ---------------------------------------------------------------- tensor helpers
+def _torch():
+    import torch  # imported lazily so that the geometry helpers work without torch
+
+    return torch
+
+
+def _dtype_code(t):
+    torch = _torch()
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise SparvarError(ERR_UNSUPPORTED, f"dtype {t.dtype} not supported")
+
+
+def _plane_stride(t, name):
+    """[B,H,rows,d] tensor with d and rows contiguous and evenly spaced planes."""
+    if t.dim() != 4:
+        raise SparvarError(ERR_INVALID, f"{name} must be [B,H,rows,d]")
+    B, H, _, d = t.shape
+    if t.stride(3) != 1 or t.stride(2) != d:
+        raise SparvarError(ERR_INVALID, f"{name} rows must be contiguous")
+    if B > 1 and t.stride(0) != H * t.stride(1):
+        raise SparvarError(ERR_INVALID, f"{name} planes must be evenly spaced")
+    return t.stride(1)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = _torch().cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _scale(softmax_scale, d):
+    return float(1.0 / math.sqrt(d) if softmax_scale is None else softmax_scale)
+
+
+# ---------------------------------------------------------------- entry points
+def sparvar_dense_attn_fwd(q, k, v, o, lse=None, softmax_scale=None, stream=None):
+    """O = softmax(scale Q K^T) V over all keys; see sparvar.h."""
+    lib = load_library()
+    B, H, n_q, d = q.shape
+    n_kv = k.shape[2]
+    if _plane_stride(v, "v") != _plane_stride(k, "k"):
+        raise SparvarError(ERR_INVALID, "k and v must share one plane stride")
+    _check(lib.sparvar_dense_attn_fwd(B, H, n_q, n_kv, d, _dtype_code(q), _ptr(q), _plane_stride(q, "q"),
+                                      _ptr(k), _ptr(v), _plane_stride(k, "k"), _ptr(o), _ptr(lse),
+                                      _scale(softmax_scale, d), _stream(stream)))
+    return o, lse
+
+
+def sparvar_select_blocks(geom, S, q_S, k_leS, lse_S, topk, topk_idx, scores_out=None, scores_in=None,
+                          softmax_scale=None, B=None, H=None, d=None, stream=None):
+    """Decision-scale pooled scores and per-query-tile top-k; see sparvar.h."""
+    lib = load_library()
+    if scores_in is None:
+        B, H, _, d = q_S.shape
+        dt = _dtype_code(q_S)
+        qs, ks = _plane_stride(q_S, "q_S"), _plane_stride(k_leS, "k_leS")
+    else:
+        B, H = scores_in.shape[0], scores_in.shape[1]
+        d = 128 if d is None else d
+        dt, qs, ks = BF16, 0, 0
+    _check(lib.sparvar_select_blocks(geom.ref, S, B, H, d, dt, _ptr(q_S), qs, _ptr(k_leS), ks, _ptr(lse_S),
+                                     _scale(softmax_scale, d), _ptr(scores_in), _ptr(scores_out), topk,
+                                     _ptr(topk_idx), _stream(stream)))
+    return topk_idx
+
+
+def sparvar_local_blocks_capacity(geom, k, radius, prev_dilation=0):
+    n = load_library().sparvar_local_blocks_capacity(geom.ref, k, radius, prev_dilation)
+    if n < 0:
+        _check(int(n))
+    return int(n)
+
+
+def sparvar_local_blocks(geom, k, radius, row_ptr, col_idx, prev_dilation=0, stream=None):
+    _check(load_library().sparvar_local_blocks(geom.ref, k, radius, prev_dilation, _ptr(row_ptr), _ptr(col_idx),
+                                               col_idx.numel(), _stream(stream)))
+    return row_ptr, col_idx
+
+
+def sparvar_map_index_capacity(geom, S, k, B, H, topk, radius, prev_dilation=0):
+    n = load_library().sparvar_map_index_capacity(geom.ref, S, k, B, H, topk, radius, prev_dilation)
+    if n < 0:
+        _check(int(n))
+    return int(n)
+
+
+def sparvar_map_index(geom, S, k, B, H, topk, topk_idx, local_row_ptr, local_col_idx, radius, row_ptr, col_idx,
+                      schedule=None, prev_dilation=0, stream=None):
+    _check(load_library().sparvar_map_index(geom.ref, S, k, B, H, topk, _ptr(topk_idx), _ptr(local_row_ptr),
+                                            _ptr(local_col_idx), radius, prev_dilation, _ptr(row_ptr),
+                                            _ptr(col_idx), col_idx.numel(), _ptr(schedule), _stream(stream)))
+    return row_ptr, col_idx, schedule
+
+
+def sparvar_block_sparse_attn_fwd(geom, k, q_k, k_lek, v_lek, o, row_ptr, col_idx, lse=None, schedule=None,
+                                  softmax_scale=None, stream=None):
+    """Block-sparse attention of scale-k queries over the kept blocks; see sparvar.h."""
+    lib = load_library()
+    B, H, _, d = q_k.shape
+    if _plane_stride(v_lek, "v_lek") != _plane_stride(k_lek, "k_lek"):
+        raise SparvarError(ERR_INVALID, "k_lek and v_lek must share one plane stride")
+    _check(lib.sparvar_block_sparse_attn_fwd(geom.ref, k, B, H, d, _dtype_code(q_k), _ptr(q_k),
+                                             _plane_stride(q_k, "q_k"), _ptr(k_lek), _ptr(v_lek),
+                                             _plane_stride(k_lek, "k_lek"), _ptr(o), _ptr(lse),
+                                             _scale(softmax_scale, d), _ptr(row_ptr), _ptr(col_idx),
+                                             _ptr(schedule), _stream(stream)))
+    return o, lse
