@@ -1,0 +1,332 @@
+"""Benchmark of the SparVAR sparse path on one MI355X.
+
+One step = one layer of the whole hot path on the Infinity 1024x1024 schedule
+(scales 1,2,4,6,8,12,16,20,24,32,40,48,64; B=2 CFG pair, H=16, d=128, bf16):
+  decision scale 32x32: dense attention + LSE, pooled block scores, top-8;
+  for each sparse step 40x40, 48x48, 64x64: local rows, index mapping into CSR,
+  block-sparse attention (8x8-token blocks, sinks = scales 1-4, 3x3 window).
+Inputs are seeded synthetic tensors resident in HBM; four input sets rotate so
+no step finds its K/V in cache from the previous one.
+
+Prints one JSON line. `value` is the algorithmic TFLOP/s of the whole step
+(4 d * kept query-key pairs, plus the decision-scale dense and scoring
+FLOPs) over the measured step time.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+SIDES = [1, 2, 4, 6, 8, 12, 16, 20, 24, 32, 40, 48, 64]
+CFG = dict(B=2, H=16, d=128, b=8, n_sink=4, S=10, steps=[11, 12, 13], topk=8, radius=1, n_freq=32)
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+N_SETS = 4
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
+    ap.add_argument("--sets", type=int, default=N_SETS)
+    return ap.parse_args()
+
+
+# ---------------------------------------------------------------- accounting
+def block_sizes(info):
+    """Token count of every block id, from the library's per-scale geometry."""
+    sizes = []
+    for l in sorted(info):
+        i = info[l]
+        for tu in range(i["tiles_h"]):
+            nr = min(i["tile_h"], i["h"] - tu * i["tile_h"])
+            for tv in range(i["tiles_w"]):
+                nc = min(i["tile_w"], i["w"] - tv * i["tile_w"])
+                sizes.append(nr * nc)
+    return np.array(sizes, dtype=np.int64)
+
+
+def query_tile_sizes(i):
+    out = []
+    for tu in range(i["tiles_h"]):
+        for tv in range(i["tiles_w"]):
+            out.append(min(i["tile_h"], i["h"] - tu * i["tile_h"]) * min(i["tile_w"], i["w"] - tv * i["tile_w"]))
+    return np.array(out, dtype=np.int64)
+
+
+def sparse_accounting(row_ptr, col_idx, info, k, BH, d, elem=2):
+    """Algorithmic FLOPs and bytes of one block-sparse attention launch."""
+    bs = block_sizes(info)
+    qsz = query_tile_sizes(info[k])
+    G = len(qsz)
+    rp = row_ptr.astype(np.int64)
+    keys = np.add.reduceat(bs[col_idx], rp[:-1]) if len(col_idx) else np.zeros(len(rp) - 1)
+    keys = np.where(np.diff(rp) > 0, keys, 0)
+    pairs = (keys * np.tile(qsz, BH)).sum()
+    flops = 4.0 * d * pairs
+    nk = info[k]["n_tokens"]
+    nb_k = info[k]["n_blocks_le"]
+    uniq_tokens = 0
+    for bh in range(BH):
+        seg = col_idx[rp[bh * G]:rp[(bh + 1) * G]]
+        uniq_tokens += bs[np.unique(seg[(seg >= 0) & (seg < nb_k)])].sum()
+    bytes_ = BH * nk * d * elem * 2 + uniq_tokens * d * elem * 2  # Q + O + unique K and V
+    density = pairs / (BH * nk * info[k]["n_tokens_le"])
+    return flops, bytes_, density, keys
+
+
+# ---------------------------------------------------------------- CPU baseline (oracle)
+def cpu_baseline(q, k, v, target_s):
+    """Time the fp64 oracle on a bounded sample of heads of the same step."""
+    import oracle as O
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    B, H, d = CFG["B"], CFG["H"], CFG["d"]
+    g = O.Geometry(SIDES, SIDES, CFG["b"], CFG["n_sink"])
+    S = CFG["S"]
+    sc = float(np.float32(1.0 / math.sqrt(d)))
+    BH = B * H
+    qf, kf, vf = (x.reshape(BH, -1, d) for x in (q, k, v))
+    flops_done = 0.0
+    heads = 0
+    t0 = time.perf_counter()
+    local = {kk: O.local_blocks(g, kk, CFG["radius"]) for kk in CFG["steps"]}
+    for bh in range(BH):
+        # decision scale: dense + pooled scores + top-k for one head
+        qS, kS, vS = qf[bh, g.C(S - 1):g.C(S)], kf[bh, :g.C(S)], vf[bh, :g.C(S)]
+        O.dense_attention(qS, kS, vS, sc)
+        scores = O.pooled_scores(qS, kS, sc, g, S)
+        tk = np.array([[O.topk_blocks(r, CFG["topk"]) for r in scores]])
+        flops_done += 4.0 * d * g.N(S) * g.C(S) + 2.0 * d * g.N(S) * g.C(S)
+        for kk in CFG["steps"]:
+            rows = O.build_rows(g, S, kk, tk, local[kk])[0]
+            O.block_sparse_attention_gather(qf[bh, g.C(kk - 1):g.C(kk)], kf[bh, :g.C(kk)], vf[bh, :g.C(kk)], g, kk,
+                                            rows, sc)
+            kept = sum(len(g.tile_local_tokens(kk, t // g.Tw(kk), t % g.Tw(kk))) *
+                       sum(len(g.block_tokens(vb)) for vb in rows[t]) for t in range(len(rows)))
+            flops_done += 4.0 * d * kept
+        heads += 1
+        if time.perf_counter() - t0 >= target_s:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": flops_done / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"whole step (decision + 3 sparse steps) for {heads} of {BH} (batch, head) planes, "
+                      f"fp64 NumPy, {dt:.1f} s"}
+
+
+def traffic_from_profile(kernel_hash):
+    """HBM bytes per launch of the sparse kernel from the committed rocprofv3 PMC
+    summary, if it was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "sparse_attn_64_traffic.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as f:
+        for line in f:
+            if "=" in line and not line.startswith("#"):
+                key, val = line.split("=", 1)
+                vals[key.strip()] = val.strip()
+    if vals.get("kernel_source_sha256") != kernel_hash:
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for name in ("attention.hip", "device_common.h", "geometry.h"):
+        with open(os.path.join(ROOT, "paper_2602_04361_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+# ---------------------------------------------------------------- main
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the path shards by (batch, head) "
+              f"with no exchange inside attention, but this build measures a single GPU.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2602_04361_amd import sparvar as sv
+    from paper_2602_04361_amd.pipeline import SparsePath
+    from paper_2602_04361_amd.synth import make_qkv
+
+    sv.load_library()
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda:0")
+    B, H, d = CFG["B"], CFG["H"], CFG["d"]
+    BH = B * H
+    g = sv.Geometry(SIDES, SIDES, CFG["b"], CFG["n_sink"])
+    sets, host0 = [], None
+    for s in range(args.sets):
+        q, k, v = make_qkv(SIDES, SIDES, B, H, d, CFG["n_freq"], CFG["n_sink"], seed=s, bf16=True)
+        if s == 0:
+            host0 = (q, k, v)
+        sets.append(tuple(torch.from_numpy(x).to(dev).to(torch.bfloat16) for x in (q, k, v)))
+        print(f"[bench] input set {s} resident", file=sys.stderr, flush=True)
+    path = SparsePath(g, CFG["S"], CFG["steps"], B, H, d, CFG["topk"], CFG["radius"])
+    info = path.info
+    stream = torch.cuda.current_stream()
+
+    names = ["dense_S", "select", "local", "map_11", "attn_11", "map_12", "attn_12", "map_13", "attn_13"]
+
+    def one_step(i, ev=None):
+        Q, K, V = sets[i % len(sets)]
+        if ev is not None:
+            ev[0].record(stream)
+        S = CFG["S"]
+        qS, kS, vS = path.q_slice(Q, S), path.kv_prefix(K, S), path.kv_prefix(V, S)
+        sv.sparvar_dense_attn_fwd(qS, kS, vS, path.o_S, path.lse_S, softmax_scale=path.scale)
+        if ev is not None:
+            ev[1].record(stream)
+        sv.sparvar_select_blocks(g, S, qS, kS, path.lse_S, path.topk, path.topk_idx, scores_out=path.scores,
+                                 softmax_scale=path.scale)
+        if ev is not None:
+            ev[2].record(stream)
+        path.build_local()
+        if ev is not None:
+            ev[3].record(stream)
+        j = 4
+        for kk in CFG["steps"]:
+            path.map_step(kk)
+            if ev is not None:
+                ev[j].record(stream)
+            path.attn_step(kk, Q, K, V)
+            if ev is not None:
+                ev[j + 1].record(stream)
+            j += 2
+
+    for i in range(args.warmup):
+        one_step(i)
+    torch.cuda.synchronize()
+
+    # accounting from the CSR built on set 0 (outside the timed region)
+    one_step(0)
+    torch.cuda.synchronize()
+    acct = {}
+    for kk in CFG["steps"]:
+        rp, ci, _ = path.csr[kk]
+        acct[kk] = sparse_accounting(rp.cpu().numpy(), ci.cpu().numpy(), info, kk, BH, d)
+    iS = info[CFG["S"]]
+    dense_S_flops = 4.0 * d * BH * iS["n_tokens"] * iS["n_tokens_le"]
+    score_flops = 2.0 * d * BH * iS["n_tokens"] * iS["n_tokens_le"]
+    step_flops = dense_S_flops + score_flops + sum(a[0] for a in acct.values())
+
+    # timed region
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(args.steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for i in range(args.steps):
+        one_step(i, evs[i])
+        evs[i][-1].record(stream)
+    end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms_step = total_ms / args.steps
+    per = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(args.steps)]))
+           for j, n in enumerate(names)}
+
+    # our dense kernel at the 64x64 step (speedup denominator), same buffers and rotation
+    i13 = info[13]
+    o_dense = torch.empty(B, H, i13["n_tokens"], d, dtype=torch.bfloat16, device=dev)
+    for i in range(3):
+        Q, K, V = sets[i % len(sets)]
+        sv.sparvar_dense_attn_fwd(path.q_slice(Q, 13), path.kv_prefix(K, 13), path.kv_prefix(V, 13), o_dense, None,
+                                  softmax_scale=path.scale)
+    torch.cuda.synchronize()
+    dn = max(3, min(args.steps, 10))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for i in range(dn):
+        Q, K, V = sets[i % len(sets)]
+        sv.sparvar_dense_attn_fwd(path.q_slice(Q, 13), path.kv_prefix(K, 13), path.kv_prefix(V, 13), o_dense, None,
+                                  softmax_scale=path.scale)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    dense64_ms = e0.elapsed_time(e1) / dn
+    dense64_flops = 4.0 * d * BH * i13["n_tokens"] * i13["n_tokens_le"]
+
+    f13, b13, dens13, _ = acct[13]
+    attn13_ms = per["attn_13"]
+    kernels = {
+        "dense_S": {"ms": per["dense_S"], "tflops": dense_S_flops / per["dense_S"] / 1e9},
+        "select": {"ms": per["select"], "tflops": score_flops / per["select"] / 1e9},
+        "local": {"ms": per["local"]},
+    }
+    for kk in CFG["steps"]:
+        f, b_, dens, keys = acct[kk]
+        side = info[kk]["h"]
+        kernels[f"map_{side}"] = {"ms": per[f"map_{kk}"]}
+        kernels[f"attn_{side}"] = {"ms": per[f"attn_{kk}"], "gflop": f / 1e9,
+                                   "tflops": f / per[f"attn_{kk}"] / 1e9,
+                                   "frac_bf16_peak": f / per[f"attn_{kk}"] / 1e9 / PEAK_BF16_TFLOPS,
+                                   "hbm_gbs_algorithmic": b_ / per[f"attn_{kk}"] / 1e6,
+                                   "density": dens, "kept_keys_per_row_mean": float(np.mean(keys))}
+    dominant = max(kernels, key=lambda n: kernels[n]["ms"])
+    traffic = traffic_from_profile(kernel_source_hash())
+    achieved = f13 / attn13_ms / 1e9
+    roofline = {"kernel": "block-sparse attention, 64x64 step", "bound": "mfma", "achieved": achieved,
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
+                "traffic": traffic, "algorithmic_bytes": b13, "algorithmic_flops": f13,
+                "dominant_kernel_in_step": dominant}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(*host0, args.cpu_seconds)
+
+    line = {
+        "metric": "ms/layer + effective TFLOP/s (% bf16 MFMA peak) sparse attn at 64x64 scale",
+        "value": step_flops / ms_step / 1e9,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) Q/K/V + 2-D sinusoidal position features + sink bias), 4 rotating sets",
+        "config": {"workload": "Infinity 1024x1024 schedule, one layer: dense+select at 32x32, "
+                               "block-sparse steps 40x40/48x48/64x64", "batch": B, "heads": H, "head_dim": d,
+                   "block": "8x8 tokens", "topk": CFG["topk"], "window_radius": CFG["radius"],
+                   "sink_scales": CFG["n_sink"], "kv_tokens_last_step": info[13]["n_tokens_le"]},
+        "ms_per_layer": ms_step,
+        "sparse_64": {"ms": attn13_ms, "tflops": achieved, "frac_bf16_peak": achieved / PEAK_BF16_TFLOPS,
+                      "density": dens13, "dense_ms": dense64_ms,
+                      "dense_tflops": dense64_flops / dense64_ms / 1e9,
+                      "speedup_vs_own_dense": dense64_ms / attn13_ms},
+        "kernels": kernels,
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line, default=lambda o: o.item() if hasattr(o, "item") else str(o)))
+
+
+if __name__ == "__main__":
+    main()
