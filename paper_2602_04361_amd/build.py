@@ -25,6 +25,8 @@ ARCH = "gfx950"
 FLAGS = [
     "-O3", "-std=c++17", f"--offload-arch={ARCH}", "-fPIC",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # keep MFMA accumulators in VGPRs (no AGPR round trips for the softmax rescale)
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
     f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}",
     "-Wall", "-Wno-unused-result",
 ]

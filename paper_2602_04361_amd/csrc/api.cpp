@@ -69,6 +69,9 @@ int build_table(const sparvar_geometry_t* g, GeoTable* T) {
       return fail(SPARVAR_ERR_INVALID, "cache longer than 2^31 tokens");
     T->C[i + 1] = (int32_t)tok;
     T->NB[i + 1] = (int32_t)blk;
+    if ((uint64_t)T->Th[i] * T->Tw[i] * T->Tw[i] >= (uint64_t(1) << 32))
+      return fail(SPARVAR_ERR_INVALID, "scale %d has too many tiles", i + 1);
+    T->mTw[i] = magic_for((uint32_t)T->Tw[i]);
   }
   return SPARVAR_OK;
 }
@@ -167,7 +170,9 @@ int sparvar_dense_attn_fwd(int32_t B, int32_t H, int32_t n_q, int32_t n_kv, int3
   a.q_bh_stride = q_bh_stride;
   a.kv_bh_stride = kv_bh_stride;
   a.softmax_scale = softmax_scale;
-  a.waves = env_int("SPARVAR_DENSE_WAVES", 0);
+  a.waves = env_int("SPARVAR_DENSE_WAVES", 8);
+  a.chunk = env_int("SPARVAR_DENSE_CHUNK", 64);
+  a.stages = env_int("SPARVAR_DENSE_STAGES", 2);
   a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
   return hip_status(launch_dense_attn(a, stream), "dense attention launch");
 }
@@ -334,6 +339,8 @@ int sparvar_block_sparse_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_
   a.col_idx = col_idx;
   a.schedule = schedule;
   a.waves = env_int("SPARVAR_SPARSE_WAVES", 0);
+  a.chunk = env_int("SPARVAR_SPARSE_CHUNK", 32);
+  a.stages = env_int("SPARVAR_SPARSE_STAGES", 3);
   a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
   return hip_status(launch_sparse_attn(a, stream), "block-sparse attention launch");
 }

@@ -38,7 +38,15 @@ __device__ __forceinline__ int32_t chunk_token(const Chunk& c, int32_t s) {
   return c.base + q * c.stride + (s - q * c.nc);
 }
 
-__device__ __forceinline__ int32_t div_magic(int32_t nc) { return (65536 + nc - 1) / nc; }
+// ceil(65536 / n) for n = 0..64 (entry 0 unused).
+__constant__ const uint32_t kNcMagic[65] = {
+    0, 65536, 32768, 21846, 16384, 13108, 10923, 9363, 8192, 7282, 6554, 5958, 5462,
+    5042, 4682, 4370, 4096, 3856, 3641, 3450, 3277, 3121, 2979, 2850, 2731, 2622,
+    2521, 2428, 2341, 2260, 2185, 2115, 2048, 1986, 1928, 1873, 1821, 1772, 1725,
+    1681, 1639, 1599, 1561, 1525, 1490, 1457, 1425, 1395, 1366, 1338, 1311, 1286,
+    1261, 1237, 1214, 1192, 1171, 1150, 1130, 1111, 1093, 1075, 1058, 1041, 1024};
+
+__device__ __forceinline__ int32_t div_magic(int32_t nc) { return kNcMagic[nc]; }
 
 __device__ __forceinline__ Chunk make_chunk(int32_t base, int32_t nc, int32_t stride, int32_t count) {
   Chunk c;

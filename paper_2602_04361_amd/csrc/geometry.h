@@ -31,7 +31,17 @@ struct GeoTable {
   int32_t Th[kMaxScales], Tw[kMaxScales];  // tiles per axis
   int32_t C[kMaxScales + 1];               // C[l] = tokens of scales 1..l
   int32_t NB[kMaxScales + 1];              // NB[l] = blocks of scales 1..l
+  uint32_t mTw[kMaxScales];                // ceil(2^32 / Tw): t / Tw == mulhi(t, mTw) for t * Tw < 2^32
 };
+
+// t / d for 0 <= t with t * d < 2^32, given m = ceil(2^32 / d) (d >= 1; m = 0 encodes d = 1).
+SV_HD uint32_t div_by_magic(uint32_t t, uint32_t m) {
+  return m == 0 ? t : (uint32_t)(((uint64_t)t * m) >> 32);
+}
+
+inline uint32_t magic_for(uint32_t d) {
+  return d <= 1 ? 0u : (uint32_t)(((uint64_t(1) << 32) + d - 1) / d);
+}
 
 // A tile of the cache: tokens base + x * stride + y for x < nr, y < nc.
 struct Tile {
@@ -61,7 +71,8 @@ SV_HD Tile tile_at(const GeoTable& G, int l, int32_t tu, int32_t tv) {
 SV_HD Tile block_tile(const GeoTable& G, int32_t v) {
   const int l = block_scale(G, v);
   const int32_t t = v - G.NB[l - 1];
-  return tile_at(G, l, t / G.Tw[l - 1], t % G.Tw[l - 1]);
+  const int32_t tu = (int32_t)div_by_magic((uint32_t)t, G.mTw[l - 1]);
+  return tile_at(G, l, tu, t - tu * G.Tw[l - 1]);
 }
 
 // Query Block Homography along one axis (appendix): nearest source tile of the

@@ -17,6 +17,8 @@ struct DenseAttnArgs {
   int64_t q_bh_stride, kv_bh_stride;
   float softmax_scale;
   int waves;    // 0 = default
+  int chunk;    // keys per chunk (32 or 64)
+  int stages;   // LDS pipeline depth
   int swizzle;  // XCD-aware workgroup order
 };
 
@@ -31,6 +33,8 @@ struct SparseAttnArgs {
   float softmax_scale;
   const int32_t *row_ptr, *col_idx, *schedule;
   int waves;    // 0 = from the tile size
+  int chunk;    // keys per chunk (32 or 64)
+  int stages;   // LDS pipeline depth
   int swizzle;
 };
 

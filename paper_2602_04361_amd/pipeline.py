@@ -20,7 +20,7 @@ from . import sparvar as sv
 
 class SparsePath:
     def __init__(self, geom: sv.Geometry, S, steps, B, H, d, topk, radius, prev_dilation=0,
-                 dtype=torch.bfloat16, device="cuda", use_schedule=True, softmax_scale=None):
+                 dtype=torch.bfloat16, device="cuda", use_schedule=False, softmax_scale=None):
         self.g = geom
         self.S, self.steps = int(S), [int(k) for k in steps]
         self.B, self.H, self.d = B, H, d

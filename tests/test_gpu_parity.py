@@ -27,7 +27,7 @@ def run_case(h, w, b, ns, S, steps, B, H, d, F, topk, r, dtype, seed=0, dil=0, h
     Qd, Kd, Vd = to_dev(q, dtype), to_dev(k, dtype), to_dev(v, dtype)
     g = sv.Geometry(h, w, b, ns)
     og = oracle_geometry(h, w, b, ns)
-    path = SparsePath(g, S, steps, B, H, d, topk, r, dil, dtype=torch_dtype(dtype))
+    path = SparsePath(g, S, steps, B, H, d, topk, r, dil, dtype=torch_dtype(dtype), use_schedule=True)
     path.build_local()
     path.decision(Qd, Kd, Vd)
     lse_k = {}
@@ -217,7 +217,7 @@ def test_deterministic_and_schedule_invariant():
     q, k, v = make_case(h, h, B, H, d, 32, 4, 11, "bf16")
     Q, K, V = to_dev(q, "bf16"), to_dev(k, "bf16"), to_dev(v, "bf16")
     g = sv.Geometry(h, h, 8, 4)
-    path = SparsePath(g, 10, [13], B, H, d, 8, 1)
+    path = SparsePath(g, 10, [13], B, H, d, 8, 1, use_schedule=True)
     path.build_local()
     path.run(Q, K, V)
     torch.cuda.synchronize()
