@@ -340,7 +340,7 @@ int sparvar_block_sparse_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_
   a.schedule = schedule;
   a.waves = env_int("SPARVAR_SPARSE_WAVES", 0);
   a.chunk = env_int("SPARVAR_SPARSE_CHUNK", 32);
-  a.stages = env_int("SPARVAR_SPARSE_STAGES", 3);
+  a.stages = env_int("SPARVAR_SPARSE_STAGES", 2);
   a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
   return hip_status(launch_sparse_attn(a, stream), "block-sparse attention launch");
 }

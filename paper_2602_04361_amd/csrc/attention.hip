@@ -350,6 +350,13 @@ typedef __attribute__((ext_vector_type(4))) short i16x4;
 typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
 typedef __attribute__((address_space(3))) void lds_void;
 
+// 16-byte direct copy HBM -> LDS: lane i of the wave writes lds + 16 i (lds is
+// wave-uniform). Kept out of lambdas: a target builtin inside a lambda voids the
+// host-side instantiation of the kernel.
+__device__ __forceinline__ void dma16(const void* g, char* lds) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void*)lds, 16, 0, 0);
+}
+
 // p points into __shared__ memory.
 __device__ __forceinline__ i16x4 lds_read_tr(const char* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(const_cast<char*>(p)));
@@ -432,16 +439,21 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
                      16 * ((4 * dt + 2 * (tr_g & 1) + (tr_q >> 1)) ^ (unit_swizzle(key) & (U - 1))) + (tr_q & 1) * 8;
   }
 
-  auto issue = [&](const Chunk& c, int s) {
-    char* kb = smem + s * kStage;
+  // Direct loads of a chunk into LDS stage S: 32-bit unsigned byte offsets from the
+  // scalar plane bases, wave-uniform LDS destinations.
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const char* kbytes = reinterpret_cast<const char*>(kplane);
+  const char* vbytes = reinterpret_cast<const char*>(vplane);
+  auto issue = [&](const Chunk& c, auto stage_c) {
+    constexpr int S = decltype(stage_c)::value;
+    char* kb = smem + S * kStage;
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
-      const int first = (j * NW + wave) * 64;
+      const int first = (j * NW + wave_s) * 64;
       const int r = ld_row[j];
-      const int32_t tok = chunk_token(c, r < c.count ? r : 0);
-      const int32_t off = tok * D + 8 * ld_unit[j];
-      __builtin_amdgcn_global_load_lds(kplane + off, (lds_void*)(kb + first * 16), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(vplane + off, (lds_void*)(kb + kTile + first * 16), 16, 0, 0);
+      const uint32_t off = (uint32_t)(chunk_token(c, r < c.count ? r : 0) * D + 8 * ld_unit[j]) * 2u;
+      dma16(kbytes + off, kb + first * 16);
+      dma16(vbytes + off, kb + kTile + first * 16);
     }
   };
 
@@ -455,20 +467,31 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
     }
   }();
   // ring of chunk descriptors: ring[0] is being computed, ring[1..] are in flight
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  using S2 = std::integral_constant<int, 2>;
+  using S3 = std::integral_constant<int, 3>;
   Chunk ring[NS - 1];
   int ahead = 0;  // chunks issued beyond the one being computed
   bool have = cur.next(ring[0]);
-  if (have) issue(ring[0], 0);
-#pragma unroll
-  for (int p = 1; p < NS - 1; ++p) {
-    if (have && ahead == p - 1 && cur.next(ring[p])) {
-      issue(ring[p], p);
+  if (have) issue(ring[0], S0{});
+  if constexpr (NS > 2) {
+    if (have && cur.next(ring[1])) {
+      issue(ring[1], S1{});
       ++ahead;
     }
   }
-  int stage = 0;
+  if constexpr (NS > 3) {
+    if (have && ahead == 1 && cur.next(ring[2])) {
+      issue(ring[2], S2{});
+      ++ahead;
+    }
+  }
 
-  while (have) {
+  // One pipeline step on LDS stage S (a compile-time constant, so every LDS
+  // address below is a lane-constant register plus an immediate).
+  auto step = [&](auto stage_c) -> bool {
+    constexpr int S = decltype(stage_c)::value;
     if (NS > 2 && ahead > 0) {
       if (ahead >= NS - 2) __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * kLoads * (NS - 2)));
       else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
@@ -479,13 +502,9 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
     const Chunk c = ring[0];
     Chunk cn;
     const bool have_n = ahead == NS - 2 && cur.next(cn);
-    if (have_n) {
-      int s_issue = stage + NS - 1;
-      if (s_issue >= NS) s_issue -= NS;
-      issue(cn, s_issue);
-    }
+    if (have_n) issue(cn, std::integral_constant<int, (S + NS - 1) % NS>{});
 
-    const char* kst = smem + stage * kStage;
+    const char* kst = smem + S * kStage;
 
     // ---- S^T = K Q^T
     f32x16 st[KC / 32];
@@ -513,7 +532,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
     for (int kt = 0; kt < KC / 32; ++kt)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, st[kt][r]);
-    mx = fmaxf(mx, xor32(mx)) * io.scale_log2;
+    mx = max_halves(mx) * io.scale_log2;
     if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.f)) {
       const float m_new = fmaxf(m_run, mx);
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
@@ -558,18 +577,24 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
     // ---- advance the ring
 #pragma unroll
     for (int p = 0; p < NS - 2; ++p) ring[p] = ring[p + 1];
-    if (have_n) {
-      ring[NS - 2] = cn;
-    } else {
-      --ahead;
+    if (have_n) ring[NS - 2] = cn;
+    else --ahead;
+    return ahead >= 0;
+  };
+
+  while (have) {
+    if (!step(S0{})) break;
+    if (!step(S1{})) break;
+    if constexpr (NS > 2) {
+      if (!step(S2{})) break;
     }
-    have = ahead >= 0;
-    if (!have_n && NS == 2) have = false;
-    stage = stage + 1 == NS ? 0 : stage + 1;
+    if constexpr (NS > 3) {
+      if (!step(S3{})) break;
+    }
   }
 
   // ---- epilogue
-  const float l_tot = l_run + xor32(l_run);
+  const float l_tot = sum_halves(l_run);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   if (qvalid) {
     const int64_t orow = (int64_t)qs.bh * io.o_rows + qrow;

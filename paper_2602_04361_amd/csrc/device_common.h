@@ -93,7 +93,33 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
-__device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32, 64); }
+// Cross-half exchange between lanes l and l ^ 32 with the gfx950 permlane32 swap:
+// after swapping x with itself, operand 0 holds the lower half's values in every
+// lane and operand 1 the upper half's. (The builtin exists only in the device
+// pass; the host pass sees a placeholder and never runs it.)
+struct HalfPair {
+  float lo, hi;
+};
+__device__ __forceinline__ HalfPair halves(float x) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return HalfPair{__uint_as_float(r[0]), __uint_as_float(r[1])};
+#else
+  return HalfPair{x, x};
+#endif
+}
+__device__ __forceinline__ float xor32(float x) {
+  const HalfPair p = halves(x);
+  return (threadIdx.x & 32) ? p.lo : p.hi;
+}
+__device__ __forceinline__ float max_halves(float x) {
+  const HalfPair p = halves(x);
+  return fmaxf(p.lo, p.hi);
+}
+__device__ __forceinline__ float sum_halves(float x) {
+  const HalfPair p = halves(x);
+  return p.lo + p.hi;
+}
 
 // Query fragments (B operand of S^T = K Q^T) for the lane's query row.
 // bf16: step s holds d in [16 s + 8 half, +8). fp32: step s holds d = 2 s + half.
