@@ -157,14 +157,19 @@ int sparvar_local_blocks(const sparvar_geometry_t* g, int32_t k, int32_t radius,
  * floor(y w_l'/w_l)), and the scale-l' tile containing it. The row is the
  * ascending, duplicate-free union of the mapped blocks and local row (a,c).
  * Row index r = (b*H + h) * G_k + g.
+ * Output layout (padded CSR): rows have a fixed stride M = (longest local row)
+ * + topk: row_ptr[r] = r * M, and col_idx[r*M .. r*M + M) holds the row's ids
+ * followed by -1 up to the stride (sparvar_block_sparse_attn_fwd skips them).
  *   topk_idx: int32 [B,H,G_S,topk] (from sparvar_select_blocks).
- *   local_row_ptr / local_col_idx: output of sparvar_local_blocks for k.
+ *   local_row_ptr / local_col_idx: output of sparvar_local_blocks for k, or
+ *   both NULL: the local rows are then generated from radius and
+ *   prev_dilation inside this call (same lists, no extra launch).
  *   row_ptr: int32 [B*H*G_k + 1]; col_idx: int32 [capacity].
- *   radius, prev_dilation: the values the local rows were built with; they
+ *   radius, prev_dilation: the values the local rows are built with; they
  *   bound the local row length (longer local rows are cut to that bound).
- *   capacity: >= sparvar_map_index_capacity(...) with the same arguments.
- *   If the rows would overflow it anyway, rows are truncated so that nothing
- *   is written beyond capacity.
+ *   capacity: >= sparvar_map_index_capacity(...) with the same arguments
+ *   (B*H*G_k * M row slots, plus B*H*G_k entries the call uses for row lengths
+ *   when a schedule is asked for).
  *   schedule (nullable): int32 [B*H*G_k], the rows ordered longest first,
  *   equal lengths in row order.
  * Requires 1 <= S < k <= num_scales.

@@ -170,7 +170,7 @@ int sparvar_dense_attn_fwd(int32_t B, int32_t H, int32_t n_q, int32_t n_kv, int3
   a.q_bh_stride = q_bh_stride;
   a.kv_bh_stride = kv_bh_stride;
   a.softmax_scale = softmax_scale;
-  a.waves = env_int("SPARVAR_DENSE_WAVES", 8);
+  a.waves = env_int("SPARVAR_DENSE_WAVES", 0);
   a.chunk = env_int("SPARVAR_DENSE_CHUNK", 64);
   a.stages = env_int("SPARVAR_DENSE_STAGES", 2);
   a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
@@ -268,7 +268,8 @@ int64_t sparvar_map_index_capacity(const sparvar_geometry_t* g, int32_t S, int32
   if (radius < 0 || prev_dilation < 0) return fail(SPARVAR_ERR_INVALID, "radius and dilation must be >= 0");
   const int32_t mx = local_max_len(T, k, radius, prev_dilation, nullptr);
   ok();
-  return (int64_t)B * H * tiles_of(T, k) * (int64_t)(mx + topk);
+  const int64_t rows = (int64_t)B * H * tiles_of(T, k);
+  return rows * (int64_t)(mx + topk) + rows;  // row entries, then per-row counts
 }
 
 int sparvar_map_index(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t B, int32_t H,
@@ -283,19 +284,20 @@ int sparvar_map_index(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t
   if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
   if (topk < 1 || topk > 1024) return fail(SPARVAR_ERR_INVALID, "topk %d outside [1, 1024]", topk);
   if (radius < 0 || prev_dilation < 0) return fail(SPARVAR_ERR_INVALID, "radius and dilation must be >= 0");
-  if (!topk_idx || !local_row_ptr || !local_col_idx || !row_ptr || !col_idx)
+  if (!topk_idx || !row_ptr || !col_idx || (!local_row_ptr) != (!local_col_idx))
     return fail(SPARVAR_ERR_INVALID, "a required pointer is NULL");
   const int32_t mx = local_max_len(T, k, radius, prev_dilation, nullptr);
   const int64_t rows = (int64_t)B * H * tiles_of(T, k);
-  const int64_t need = rows * (int64_t)(mx + topk);
+  const int64_t bound = rows * (int64_t)(mx + topk);
+  const int64_t need = bound + rows;
   if (rows >= (int64_t(1) << 31) || need >= (int64_t(1) << 31))
     return fail(SPARVAR_ERR_INVALID, "index lists too large for int32 offsets");
   if (capacity < need)
     return fail(SPARVAR_ERR_CAPACITY, "capacity %lld < bound %lld", (long long)capacity, (long long)need);
   if ((int64_t)(mx + topk) * 2 * 4 * 4 > 64 * 1024)
     return fail(SPARVAR_ERR_UNSUPPORTED, "rows of %d candidates exceed the merge kernel's LDS", mx + topk);
-  return hip_status(launch_map_index(T, S, k, B * H, topk, topk_idx, local_row_ptr, local_col_idx, mx, row_ptr,
-                                     col_idx, capacity, schedule, stream),
+  return hip_status(launch_map_index(T, S, k, B * H, topk, topk_idx, local_row_ptr, local_col_idx, radius,
+                                     prev_dilation, mx, row_ptr, col_idx, bound, schedule, stream),
                     "map index launch");
 }
 

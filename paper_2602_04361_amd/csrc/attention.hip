@@ -340,32 +340,7 @@ __device__ __forceinline__ int32_t swizzled_item(int32_t wg, int32_t n_wg, int32
   return (wg & 7) * per + (wg >> 3);
 }
 
-// Row r's 16-byte unit u lives at unit u ^ unit_swizzle(r) (bijection on 0..15).
-// Sixteen consecutive rows read at one logical unit hit sixteen different
-// units, and four consecutive rows x two adjacent units (a transposing read)
-// hit eight different units.
-__device__ __forceinline__ int unit_swizzle(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
-
-typedef __attribute__((ext_vector_type(4))) short i16x4;
-typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-typedef __attribute__((address_space(3))) void lds_void;
-
-// 16-byte direct copy HBM -> LDS: lane i of the wave writes lds + 16 i (lds is
-// wave-uniform). Kept out of lambdas: a target builtin inside a lambda voids the
-// host-side instantiation of the kernel.
-__device__ __forceinline__ void dma16(const void* g, char* lds) {
-  __builtin_amdgcn_global_load_lds(g, (lds_void*)lds, 16, 0, 0);
-}
-
-// p points into __shared__ memory.
-__device__ __forceinline__ i16x4 lds_read_tr(const char* p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(const_cast<char*>(p)));
-}
-
 // ---------------------------------------------------------------- bf16 kernel
-// s_waitcnt immediate for "vmcnt <= n" (gfx9 encoding; expcnt and lgkmcnt left at max).
-__host__ __device__ constexpr int waitcnt_vm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
-
 template <int D, int NW, int KC, int NS, class Src>
 __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) {
   constexpr int NT = NW * 64;
@@ -827,9 +802,22 @@ void shape_for(int d, int nw, int want_kc, int want_ns, int* kc, int* ns) {
 }  // namespace
 
 hipError_t launch_dense_attn(const DenseAttnArgs& a, hipStream_t stream) {
-  const int nw = a.waves > 0 ? a.waves : 4;
+  // Widest workgroup (most queries sharing each K/V chunk) that still gives every
+  // one of the 256 CUs a workgroup: 8 waves, else 4 waves, else 2 waves with
+  // 32-key chunks.
+  auto wgs = [&](int w) { return (int64_t)a.BH * ((a.n_q + 32 * w - 1) / (32 * w)); };
+  int nw = a.waves;
+  int want_kc = a.chunk;
+  if (nw <= 0) {
+    if (wgs(8) >= 256) nw = 8;
+    else if (wgs(4) >= 256) nw = 4;
+    else {
+      nw = 2;
+      want_kc = 32;
+    }
+  }
   int kc = 64, ns = 2;
-  if (a.bf16) shape_for(a.d, nw, a.chunk, a.stages, &kc, &ns);
+  if (a.bf16) shape_for(a.d, nw, want_kc, a.stages, &kc, &ns);
   const int32_t qpw = nw * kQPerWave;
   AttnIO io;
   io.q = a.q;

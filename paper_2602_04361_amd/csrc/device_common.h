@@ -188,4 +188,29 @@ __device__ __forceinline__ int key_of(int kt, int r, int half) {
 // Uniform (wave-invariant) value hint.
 __device__ __forceinline__ int32_t uniform(int32_t x) { return __builtin_amdgcn_readfirstlane(x); }
 
+// Row r's 16-byte unit u lives at unit u ^ unit_swizzle(r) (bijection on 0..15).
+// Sixteen consecutive rows read at one logical unit hit sixteen different
+// units, and four consecutive rows x two adjacent units (a transposing read)
+// hit eight different units.
+__device__ __forceinline__ int unit_swizzle(int r) { return ((r & 3) << 2) | ((r >> 2) & 3); }
+
+typedef __attribute__((ext_vector_type(4))) short i16x4;
+typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+typedef __attribute__((address_space(3))) void lds_void;
+
+// 16-byte direct copy HBM -> LDS: lane i of the wave writes lds + 16 i (lds is
+// wave-uniform). Kept out of lambdas: a target builtin inside a lambda voids the
+// host-side instantiation of the kernel.
+__device__ __forceinline__ void dma16(const void* g, char* lds) {
+  __builtin_amdgcn_global_load_lds(g, (lds_void*)lds, 16, 0, 0);
+}
+
+// p points into __shared__ memory.
+__device__ __forceinline__ i16x4 lds_read_tr(const char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(const_cast<char*>(p)));
+}
+
+// s_waitcnt immediate for "vmcnt <= n" (gfx9 encoding; expcnt and lgkmcnt left at max).
+__host__ __device__ constexpr int waitcnt_vm(int n) { return (n & 15) | (7 << 4) | (15 << 8) | ((n >> 4) << 14); }
+
 }  // namespace sparvar

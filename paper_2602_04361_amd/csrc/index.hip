@@ -2,14 +2,14 @@
 //
 // local_blocks_kernel (one workgroup): row lengths -> prefix sum -> entries of
 //   the sink + cross-scale local rows (block form of the CSLA window, Sec. 3.3).
-// map_rows_kernel (one wave per CSR row, two passes): candidates are the local
-//   row of the target tile plus the Decompose-Align-Project image of every
-//   block selected for the source tile given by the Query Block Homography
-//   (appendix, Cross-Scale Sparse Index Mapping). Pass 0 counts distinct
-//   candidates; pass 1 writes each distinct candidate at its rank, giving an
-//   ascending duplicate-free row.
-// scan_schedule_kernel (one workgroup): row lengths -> row_ptr (clamped to the
-//   index capacity) and, optionally, a longest-first stable row order.
+// map_rows_kernel (one wave per row): candidates are the local row of the
+//   target tile plus the Decompose-Align-Project image of every block selected
+//   for the source tile given by the Query Block Homography (appendix,
+//   Cross-Scale Sparse Index Mapping). Each distinct candidate is written at its
+//   rank, so the row is ascending and duplicate-free; rows sit at a fixed stride
+//   (the largest possible row) and end with -1 padding, so no prefix sum and a
+//   single launch build them.
+// schedule_kernel (optional): the rows' longest-first stable order.
 #include "device_common.h"
 #include "launch.h"
 
@@ -61,19 +61,23 @@ __global__ __launch_bounds__(kScanThreads) void local_blocks_kernel(GeoTable G, 
 struct MapIO {
   GeoTable G;
   const int32_t* topk_idx;
-  const int32_t* local_row_ptr;
+  const int32_t* local_row_ptr;  // NULL: local rows come from (radius, dil)
   const int32_t* local_col;
   int32_t* row_ptr;
   int32_t* col_idx;
-  int32_t S, k, G_k, G_S, topk, rows, max_cand;
+  int32_t* counts;     // [rows] row lengths (only written when a schedule is asked for)
+  int32_t* schedule;   // nullable
+  int32_t S, k, G_k, G_S, topk, rows, max_cand, radius, dil;
 };
 
 constexpr int kMapWaves = 4;
 constexpr int32_t kInvalid = 0x7fffffff;
 
-template <int PASS>
+// One wave per row: candidates (local row + mapped selection) in LDS, first
+// occurrences kept, each kept id written at its rank; the row occupies
+// col_idx[r * max_cand, (r + 1) * max_cand) with -1 after its last id.
 __global__ __launch_bounds__(kMapWaves * 64) void map_rows_kernel(MapIO io) {
-  extern __shared__ int32_t s_cand[];  // [kMapWaves][2][max_cand]: candidates, first occurrences
+  extern __shared__ int32_t s_cand[];  // [kMapWaves][2][max_cand]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int32_t r = blockIdx.x * kMapWaves + wave;
   const bool active = r < io.rows;
@@ -86,20 +90,24 @@ __global__ __launch_bounds__(kMapWaves * 64) void map_rows_kernel(MapIO io) {
   const int32_t gs = homography(a, G.Th[io.k - 1], G.Th[io.S - 1]) * G.Tw[io.S - 1] +
                      homography(c, twk, G.Tw[io.S - 1]);
   int32_t lp = 0, n_loc = 0;
+  const LocalRow lr = local_row(G, io.k, io.radius, io.dil, active ? g : 0);
   if (active) {
-    lp = io.local_row_ptr[g];
-    n_loc = io.local_row_ptr[g + 1] - lp;
+    if (io.local_row_ptr) {
+      lp = io.local_row_ptr[g];
+      n_loc = io.local_row_ptr[g + 1] - lp;
+    } else {
+      n_loc = local_row_len(lr);
+    }
     if (n_loc < 0) n_loc = 0;
     if (n_loc > io.max_cand - io.topk) n_loc = io.max_cand - io.topk;
   }
   const int32_t n = active ? n_loc + io.topk : 0;
   const int32_t* sel = io.topk_idx + ((int64_t)bh * io.G_S + gs) * io.topk;
   const int32_t nb_S = G.NB[io.S], nb_k = G.NB[io.k];
-
   for (int32_t i = lane; i < n; i += 64) {
     int32_t v;
     if (i < n_loc) {
-      v = io.local_col[lp + i];
+      v = io.local_row_ptr ? io.local_col[lp + i] : local_row_entry(G, io.k, lr, i);
       if (v < 0 || v >= nb_k) v = kInvalid;
     } else {
       const int32_t s = sel[i - n_loc];
@@ -108,89 +116,55 @@ __global__ __launch_bounds__(kMapWaves * 64) void map_rows_kernel(MapIO io) {
     cand[i] = v;
   }
   __syncthreads();
-  int32_t kept = 0;
+  // first occurrences (branch-free scan so the LDS reads pipeline)
   for (int32_t i = lane; i < n; i += 64) {
     const int32_t v = cand[i];
-    bool keep = v != kInvalid;
-    for (int32_t j = 0; j < i && keep; ++j) keep = cand[j] != v;
-    uniq[i] = keep ? v : kInvalid;
-    kept += keep;
-  }
-  if (PASS == 0) {
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) kept += __shfl_xor(kept, off, 64);
-    if (active && lane == 0) io.row_ptr[r + 1] = kept;
-    if (r == 0 && lane == 0) io.row_ptr[0] = 0;
-    return;
+    int32_t dup = 0;
+#pragma unroll 8
+    for (int32_t j = 0; j < n; ++j) dup |= (j < i) & (cand[j] == v);
+    uniq[i] = (dup || v == kInvalid) ? kInvalid : v;
   }
   __syncthreads();
-  if (!active) return;
-  const int32_t start = io.row_ptr[r], stop = io.row_ptr[r + 1];
-  for (int32_t i = lane; i < n; i += 64) {
-    const int32_t v = uniq[i];
-    if (v == kInvalid) continue;
-    int32_t rank = 0;  // distinct kept values below v
-    for (int32_t j = 0; j < n; ++j) rank += uniq[j] < v;
-    if (start + rank < stop) io.col_idx[start + rank] = v;
+  int32_t kept = 0;
+  if (active) {
+    int32_t* out = io.col_idx + (int64_t)r * io.max_cand;
+    for (int32_t i = lane; i < n; i += 64) {
+      const int32_t v = uniq[i];
+      int32_t rank = 0;  // distinct kept values below v
+#pragma unroll 8
+      for (int32_t j = 0; j < n; ++j) rank += uniq[j] < v;
+      if (v != kInvalid) {
+        out[rank] = v;
+        ++kept;
+      }
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) kept += __shfl_xor(kept, off, 64);
+    for (int32_t i = kept + lane; i < io.max_cand; i += 64) out[i] = -1;
+    if (lane == 0) {
+      io.row_ptr[r] = r * io.max_cand;
+      if (r == io.rows - 1) io.row_ptr[io.rows] = io.rows * io.max_cand;
+      if (io.schedule) io.counts[r] = kept;
+    }
   }
 }
 
-// Longest-first stable order of rows given row_ptr. Counting sort by length
-// (descending); ties keep row order: within a chunk of kScanThreads rows,
-// waves are placed one after another, and inside a wave a row's rank among
-// equal lengths comes from ballots.
-__global__ __launch_bounds__(kScanThreads) void scan_schedule_kernel(int32_t* row_ptr, int32_t rows,
-                                                                     int64_t capacity,
-                                                                     int32_t* schedule,
-                                                                     int32_t max_len) {
-  __shared__ int32_t lds[kScanThreads];
-  extern __shared__ int32_t s_hist[];  // [max_len + 1] start offsets, then running counts
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  block_inclusive_scan(row_ptr + 1, rows, capacity, lds);
-  __syncthreads();
-  if (!schedule) return;
-  int32_t* hist = s_hist;
-  for (int32_t i = tid; i <= max_len; i += kScanThreads) hist[i] = 0;
-  __syncthreads();
-  for (int32_t r = tid; r < rows; r += kScanThreads) {
-    int32_t len = row_ptr[r + 1] - row_ptr[r];
-    len = len > max_len ? max_len : len;
-    atomicAdd(&hist[len], 1);
+// Longest-first stable order: rank of row r = rows that are longer, plus rows
+// of equal length with a smaller index.
+__global__ __launch_bounds__(kMapWaves * 64) void schedule_kernel(const int32_t* counts, int32_t rows,
+                                                                  int32_t* schedule) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int32_t r = blockIdx.x * kMapWaves + wave;
+  if (r >= rows) return;
+  const int32_t len = counts[r];
+  int32_t before = 0;
+  for (int32_t i = lane; i < rows; i += 64) {
+    const int32_t li = counts[i];
+    before += (li > len) || (li == len && i < r);
   }
-  __syncthreads();
-  if (tid == 0) {  // exclusive offsets, longest first
-    int32_t run = 0;
-    for (int32_t len = max_len; len >= 0; --len) {
-      const int32_t h = hist[len];
-      hist[len] = run;
-      run += h;
-    }
-  }
-  __syncthreads();
-  int nbits = 1;
-  while ((1 << nbits) <= max_len) ++nbits;
-  for (int32_t c0 = 0; c0 < rows; c0 += kScanThreads) {
-    const int32_t r = c0 + tid;
-    const bool live = r < rows;
-    int32_t len = live ? row_ptr[r + 1] - row_ptr[r] : 0;
-    len = len > max_len ? max_len : len;
-    uint64_t same = __ballot(live);
-    for (int b = 0; b < nbits; ++b) {
-      const uint64_t bit = __ballot(live && ((len >> b) & 1));
-      same &= ((len >> b) & 1) ? bit : ~bit;
-    }
-    const uint64_t below = same & ((1ull << lane) - 1ull);
-    const int rank = __popcll(below);
-    const bool last = (same >> lane) == 1ull;  // highest lane with this length
-    for (int w = 0; w < kScanThreads / 64; ++w) {
-      if (wave == w && live) {
-        schedule[hist[len] + rank] = r;
-      }
-      __syncthreads();
-      if (wave == w && live && last) hist[len] += rank + 1;
-      __syncthreads();
-    }
-  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) before += __shfl_xor(before, off, 64);
+  if (lane == 0) schedule[before] = r;
 }
 
 hipError_t launch_local_blocks(const GeoTable& G, int k, int32_t radius, int32_t dil, int32_t* row_ptr,
@@ -202,8 +176,9 @@ hipError_t launch_local_blocks(const GeoTable& G, int k, int32_t radius, int32_t
 
 hipError_t launch_map_index(const GeoTable& G, int S, int k, int32_t BH, int32_t topk,
                             const int32_t* topk_idx, const int32_t* local_row_ptr,
-                            const int32_t* local_col_idx, int32_t max_local, int32_t* row_ptr,
-                            int32_t* col_idx, int64_t capacity, int32_t* schedule, hipStream_t stream) {
+                            const int32_t* local_col_idx, int32_t radius, int32_t dil, int32_t max_local,
+                            int32_t* row_ptr, int32_t* col_idx, int64_t entries_bound, int32_t* schedule,
+                            hipStream_t stream) {
   MapIO io;
   io.G = G;
   io.topk_idx = topk_idx;
@@ -218,18 +193,17 @@ hipError_t launch_map_index(const GeoTable& G, int S, int k, int32_t BH, int32_t
   io.topk = topk;
   io.rows = BH * io.G_k;
   io.max_cand = max_local + topk;
+  io.radius = radius;
+  io.dil = dil;
+  io.counts = col_idx + entries_bound;  // past the last row slot
+  io.schedule = schedule;
   if (io.rows == 0) return hipSuccess;
   const int32_t grid = (io.rows + kMapWaves - 1) / kMapWaves;
   const size_t shmem = (size_t)kMapWaves * 2 * io.max_cand * sizeof(int32_t);
-  hipLaunchKernelGGL(map_rows_kernel<0>, dim3(grid), dim3(kMapWaves * 64), shmem, stream, io);
+  hipLaunchKernelGGL(map_rows_kernel, dim3(grid), dim3(kMapWaves * 64), shmem, stream, io);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  const int32_t max_len = io.max_cand;
-  hipLaunchKernelGGL(scan_schedule_kernel, dim3(1), dim3(kScanThreads), (size_t)(max_len + 1) * sizeof(int32_t),
-                     stream, row_ptr, io.rows, capacity, schedule, max_len);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(map_rows_kernel<1>, dim3(grid), dim3(kMapWaves * 64), shmem, stream, io);
+  if (e != hipSuccess || !schedule) return e;
+  hipLaunchKernelGGL(schedule_kernel, dim3(grid), dim3(kMapWaves * 64), 0, stream, io.counts, io.rows, schedule);
   return hipGetLastError();
 }
 

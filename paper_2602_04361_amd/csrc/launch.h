@@ -58,7 +58,8 @@ hipError_t launch_local_blocks(const GeoTable& G, int k, int32_t radius, int32_t
                                int32_t* col_idx, hipStream_t stream);
 hipError_t launch_map_index(const GeoTable& G, int S, int k, int32_t BH, int32_t topk,
                             const int32_t* topk_idx, const int32_t* local_row_ptr,
-                            const int32_t* local_col_idx, int32_t max_local, int32_t* row_ptr,
-                            int32_t* col_idx, int64_t capacity, int32_t* schedule, hipStream_t stream);
+                            const int32_t* local_col_idx, int32_t radius, int32_t dil, int32_t max_local,
+                            int32_t* row_ptr, int32_t* col_idx, int64_t entries_bound, int32_t* schedule,
+                            hipStream_t stream);
 
 }  // namespace sparvar

@@ -23,6 +23,7 @@ struct ScoreIO {
   float* scores;
   int64_t q_bh_stride, k_bh_stride;
   int32_t S, G_S, NB;
+  int32_t per;  // blocks per workgroup along grid.y (bf16 scoring)
   float scale_log2;
 };
 
@@ -32,8 +33,9 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
+// fp32 (parity-grade) scoring: K rows read straight from memory, one reduction per block.
 template <typename T, int D, int NW>
-__global__ __launch_bounds__(NW * 64) void pooled_scores_kernel(ScoreIO io) {
+__global__ __launch_bounds__(NW * 64) void pooled_scores_f32_kernel(ScoreIO io) {
   constexpr bool kBF16 = std::is_same<T, bf16_bits>::value;
   __shared__ float red[NW];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -90,6 +92,180 @@ __global__ __launch_bounds__(NW * 64) void pooled_scores_kernel(ScoreIO io) {
   }
 }
 
+// Blocks 0..NB-1 of scales 1..S in id order, each cut into bands of whole tile
+// rows of at most KC keys (a block never shares a chunk with another block).
+template <int KC>
+struct BlockWalker {
+  const GeoTable* G;
+  int32_t l, tu, tv, r0, v, nb;
+  Tile t;
+  // walk blocks [first, end)
+  __device__ __forceinline__ void start(const GeoTable* g, int32_t first, int32_t end) {
+    G = g;
+    nb = end;
+    v = first;
+    r0 = 0;
+    if (v < nb) {
+      l = block_scale(*G, v);
+      const int32_t t0 = v - G->NB[l - 1];
+      tu = (int32_t)div_by_magic((uint32_t)t0, G->mTw[l - 1]);
+      tv = t0 - tu * G->Tw[l - 1];
+      t = tile_at(*G, l, tu, tv);
+    }
+  }
+  // Next chunk; `blk` is its block id and `last` tells whether it ends that block.
+  __device__ __forceinline__ bool next(Chunk& c, int32_t& blk, bool& last) {
+    if (v >= nb) return false;
+    const int32_t rpc = KC / t.nc;  // t.nc <= block edge <= 64 = KC
+    const int32_t rows = (t.nr - r0 < rpc) ? t.nr - r0 : rpc;
+    c = make_chunk(t.base + r0 * t.stride, t.nc, t.stride, rows * t.nc);
+    blk = v;
+    r0 += rows;
+    last = r0 >= t.nr;
+    if (last) {
+      ++v;
+      r0 = 0;
+      if (++tv == G->Tw[l - 1]) {
+        tv = 0;
+        if (++tu == G->Th[l - 1]) {
+          tu = 0;
+          ++l;
+        }
+      }
+      if (v < nb) t = tile_at(*G, l, tu, tv);
+    }
+    return true;
+  }
+};
+
+// bf16 scoring: one workgroup per (b, h, query tile g of scale S). K chunks stream
+// HBM -> LDS (direct 16-byte loads, swizzled rows, double buffered); S^T = K Q^T
+// on MFMA; each lane accumulates exp2(scale*log2e*s - lse*log2e) over its keys
+// and its query; at the end of a block the wave sum goes to LDS, and the final
+// score is the sum over waves in order (deterministic).
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64) void pooled_scores_kernel(ScoreIO io) {
+  constexpr int KC = 64, NT = NW * 64, U = D / 8, kRow = D * 2, kTile = KC * kRow;
+  constexpr int kLoads = KC * U / NT;
+  static_assert((KC * U) % NT == 0, "chunk must split evenly over the workgroup");
+  __shared__ __attribute__((aligned(16))) char smem[2 * kTile];
+  extern __shared__ float red[];  // [NW][NB] per-wave block sums
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int l32 = lane & 31, half = lane >> 5;
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  const int32_t row = blockIdx.x;  // (b*H + h) * G_S + g
+  const int32_t bh = row / io.G_S, g = row - bh * io.G_S;
+  const GeoTable& G = io.G;
+  const int S = io.S;
+  const int32_t tw = G.Tw[S - 1];
+  const Tile qt = tile_at(G, S, g / tw, g % tw);
+  const int32_t nq = qt.nr * qt.nc;
+  const int32_t qslot = wave * kQPerWave + l32;
+  const bool qvalid = qslot < nq;
+  const int32_t qi = qvalid ? qslot : 0;
+  const int32_t qrow = (qt.base - G.C[S - 1]) + (qi / qt.nc) * qt.stride + (qi % qt.nc);
+  const bf16_bits* qplane = static_cast<const bf16_bits*>(io.q) + (int64_t)bh * io.q_bh_stride;
+  const char* kbytes = reinterpret_cast<const char*>(static_cast<const bf16_bits*>(io.k) + (int64_t)bh * io.k_bh_stride);
+  QFragBF16<D> qf;
+  qf.load(qplane + (int64_t)qrow * D, half);
+  const float lse2 = io.lse[(int64_t)bh * G.h[S - 1] * G.w[S - 1] + qrow] * kLog2e;
+
+  int ld_row[kLoads], ld_unit[kLoads];
+#pragma unroll
+  for (int j = 0; j < kLoads; ++j) {
+    const int slot = (j * NW + wave) * 64 + lane;
+    ld_row[j] = slot / U;
+    ld_unit[j] = (slot % U) ^ (unit_swizzle(ld_row[j]) & (U - 1));
+  }
+  int k_off[2][D / 16];
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt) {
+    const int r = 32 * kt + l32;
+#pragma unroll
+    for (int s2 = 0; s2 < D / 16; ++s2) k_off[kt][s2] = r * kRow + 16 * ((2 * s2 + half) ^ (unit_swizzle(r) & (U - 1)));
+  }
+  auto issue = [&](const Chunk& c, auto stage_c) {
+    constexpr int SG = decltype(stage_c)::value;
+#pragma unroll
+    for (int j = 0; j < kLoads; ++j) {
+      const int first = (j * NW + wave_s) * 64;
+      const int r = ld_row[j];
+      const uint32_t off = (uint32_t)(chunk_token(c, r < c.count ? r : 0) * D + 8 * ld_unit[j]) * 2u;
+      dma16(kbytes + off, smem + SG * kTile + first * 16);
+    }
+  };
+
+  // this workgroup scores blocks [v0, v1)
+  const int32_t per = io.per;
+  const int32_t v0 = blockIdx.y * per;
+  const int32_t v1 = (v0 + per < io.NB) ? v0 + per : io.NB;
+  BlockWalker<KC> walk;
+  walk.start(&G, v0, v1);
+  Chunk c0;
+  int32_t b0 = 0;
+  bool last0 = false;
+  bool have = walk.next(c0, b0, last0);
+  if (have) issue(c0, std::integral_constant<int, 0>{});
+  float psum = 0.f;
+
+  auto step = [&](auto stage_c) -> bool {
+    constexpr int SG = decltype(stage_c)::value;
+    __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    __syncthreads();
+    Chunk cn;
+    int32_t bn = 0;
+    bool lastn = false;
+    const bool have_n = walk.next(cn, bn, lastn);
+    if (have_n) issue(cn, std::integral_constant<int, SG ^ 1>{});
+    const char* kst = smem + SG * kTile;
+    f32x16 st[2];
+    st[0] = zero16();
+    st[1] = zero16();
+#pragma unroll
+    for (int s2 = 0; s2 < D / 16; ++s2) {
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt) {
+        const u32x4 a = *reinterpret_cast<const u32x4*>(kst + k_off[kt][s2]);
+        st[kt] = mfma_bf16(as_bf16x8(a), qf.f[s2], st[kt]);
+      }
+    }
+    float part = 0.f;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(st[kt][r], io.scale_log2, -lse2));
+        part += key_of(kt, r, half) < c0.count ? p : 0.f;
+      }
+    }
+    psum += qvalid ? part : 0.f;
+    if (last0) {
+      float s = psum;
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
+      if (lane == 0) red[wave * per + (b0 - v0)] = s;
+      psum = 0.f;
+    }
+    c0 = cn;
+    b0 = bn;
+    last0 = lastn;
+    return have_n;
+  };
+  while (have) {
+    if (!step(std::integral_constant<int, 0>{})) break;
+    if (!step(std::integral_constant<int, 1>{})) break;
+  }
+  __syncthreads();
+  float* out = io.scores + (int64_t)row * io.NB;
+  for (int32_t v = v0 + tid; v < v1; v += NT) {
+    float sc = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) sc += red[w * per + (v - v0)];
+    out[v] = sc;
+  }
+}
+
 __global__ __launch_bounds__(64) void topk_kernel(const float* __restrict__ scores, int32_t nb,
                                                   int32_t topk, int32_t* __restrict__ out) {
   extern __shared__ float s_sc[];
@@ -123,12 +299,32 @@ __global__ __launch_bounds__(64) void topk_kernel(const float* __restrict__ scor
 
 namespace {
 template <typename T, int D>
-hipError_t launch_scores_t(const ScoreIO& io, int nw, int32_t grid, hipStream_t stream) {
+hipError_t launch_scores_f32(const ScoreIO& io, int nw, int32_t grid, hipStream_t stream) {
   switch (nw) {
-    case 1: hipLaunchKernelGGL((pooled_scores_kernel<T, D, 1>), dim3(grid), dim3(64), 0, stream, io); break;
-    case 2: hipLaunchKernelGGL((pooled_scores_kernel<T, D, 2>), dim3(grid), dim3(128), 0, stream, io); break;
-    case 4: hipLaunchKernelGGL((pooled_scores_kernel<T, D, 4>), dim3(grid), dim3(256), 0, stream, io); break;
-    default: hipLaunchKernelGGL((pooled_scores_kernel<T, D, 8>), dim3(grid), dim3(512), 0, stream, io); break;
+    case 1: hipLaunchKernelGGL((pooled_scores_f32_kernel<T, D, 1>), dim3(grid), dim3(64), 0, stream, io); break;
+    case 2: hipLaunchKernelGGL((pooled_scores_f32_kernel<T, D, 2>), dim3(grid), dim3(128), 0, stream, io); break;
+    case 4: hipLaunchKernelGGL((pooled_scores_f32_kernel<T, D, 4>), dim3(grid), dim3(256), 0, stream, io); break;
+    default: hipLaunchKernelGGL((pooled_scores_f32_kernel<T, D, 8>), dim3(grid), dim3(512), 0, stream, io); break;
+  }
+  return hipGetLastError();
+}
+// Blocks of a row are split over grid.y so that about 2048 workgroups run.
+template <int D>
+hipError_t launch_scores_bf16(const ScoreIO& io, int nw, int32_t grid, hipStream_t stream) {
+  int32_t splits = (2048 + grid - 1) / grid;
+  if (splits > io.NB) splits = io.NB;
+  if (splits < 1) splits = 1;
+  const int32_t per = (io.NB + splits - 1) / splits;
+  splits = (io.NB + per - 1) / per;
+  ScoreIO io2 = io;
+  io2.per = per;
+  const size_t red = (size_t)nw * per * sizeof(float);
+  const dim3 g(grid, splits);
+  switch (nw) {
+    case 1: hipLaunchKernelGGL((pooled_scores_kernel<D, 1>), g, dim3(64), red, stream, io2); break;
+    case 2: hipLaunchKernelGGL((pooled_scores_kernel<D, 2>), g, dim3(128), red, stream, io2); break;
+    case 4: hipLaunchKernelGGL((pooled_scores_kernel<D, 4>), g, dim3(256), red, stream, io2); break;
+    default: hipLaunchKernelGGL((pooled_scores_kernel<D, 8>), g, dim3(512), red, stream, io2); break;
   }
   return hipGetLastError();
 }
@@ -148,14 +344,17 @@ hipError_t launch_pooled_scores(const ScoreArgs& a, hipStream_t stream) {
   io.S = S;
   io.G_S = tiles_of(G, S);
   io.NB = G.NB[S];
+  io.per = io.NB;
   io.scale_log2 = a.softmax_scale * kLog2e;
   const int32_t tile_q = G.eh[S - 1] * G.ew[S - 1];
   const int nw = tile_q <= 32 ? 1 : tile_q <= 64 ? 2 : tile_q <= 128 ? 4 : 8;
   const int32_t grid = a.BH * io.G_S;
   if (grid == 0) return hipSuccess;
-  if (a.bf16) return a.d == 64 ? launch_scores_t<bf16_bits, 64>(io, nw, grid, stream)
-                               : launch_scores_t<bf16_bits, 128>(io, nw, grid, stream);
-  return a.d == 64 ? launch_scores_t<float, 64>(io, nw, grid, stream) : launch_scores_t<float, 128>(io, nw, grid, stream);
+  if (a.bf16 && (size_t)nw * io.NB * sizeof(float) <= 32 * 1024)
+    return a.d == 64 ? launch_scores_bf16<64>(io, nw, grid, stream) : launch_scores_bf16<128>(io, nw, grid, stream);
+  if (a.bf16) return a.d == 64 ? launch_scores_f32<bf16_bits, 64>(io, nw, grid, stream)
+                               : launch_scores_f32<bf16_bits, 128>(io, nw, grid, stream);
+  return a.d == 64 ? launch_scores_f32<float, 64>(io, nw, grid, stream) : launch_scores_f32<float, 128>(io, nw, grid, stream);
 }
 
 hipError_t launch_topk(const float* scores, int32_t rows, int32_t nb, int32_t topk, int32_t* out,

@@ -20,12 +20,15 @@ from . import sparvar as sv
 
 class SparsePath:
     def __init__(self, geom: sv.Geometry, S, steps, B, H, d, topk, radius, prev_dilation=0,
-                 dtype=torch.bfloat16, device="cuda", use_schedule=False, softmax_scale=None):
+                 dtype=torch.bfloat16, device="cuda", use_schedule=False, softmax_scale=None, local_lists=False):
         self.g = geom
         self.S, self.steps = int(S), [int(k) for k in steps]
         self.B, self.H, self.d = B, H, d
         self.topk, self.radius, self.dil = topk, radius, prev_dilation
         self.dtype, self.device = dtype, device
+        # local_lists: build the sink + local rows once with sparvar_local_blocks and
+        # pass them to the mapping; otherwise the mapping generates them itself.
+        self.local_lists = local_lists
         self.scale = float(torch.tensor(1.0 / math.sqrt(d), dtype=torch.float32)) if softmax_scale is None \
             else float(softmax_scale)
         info = {l: geom.scale_info(l) for l in range(1, len(geom.h) + 1)}
@@ -70,7 +73,7 @@ class SparsePath:
                                  softmax_scale=self.scale)
 
     def map_step(self, k):
-        rp_l, ci_l = self.local[k]
+        rp_l, ci_l = self.local[k] if self.local_lists else (None, None)
         rp, ci, sch = self.csr[k]
         sv.sparvar_map_index(self.g, self.S, k, self.B, self.H, self.topk, self.topk_idx, rp_l, ci_l, self.radius,
                              rp, ci, schedule=sch, prev_dilation=self.dil)
@@ -86,7 +89,7 @@ class SparsePath:
         self.attn_step(k, Q_all, K_all, V_all)
 
     def run(self, Q_all, K_all, V_all):
-        """Decision step plus every sparse step (local rows must be built)."""
+        """Decision step plus every sparse step (with local_lists, build_local() first)."""
         self.decision(Q_all, K_all, V_all)
         for k in self.steps:
             self.step(k, Q_all, K_all, V_all)

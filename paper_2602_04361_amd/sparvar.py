@@ -215,6 +215,7 @@ def sparvar_map_index_capacity(geom, S, k, B, H, topk, radius, prev_dilation=0):
 
 def sparvar_map_index(geom, S, k, B, H, topk, topk_idx, local_row_ptr, local_col_idx, radius, row_ptr, col_idx,
                       schedule=None, prev_dilation=0, stream=None):
+    """Mapped + local blocks -> CSR; local_row_ptr/local_col_idx may both be None."""
     _check(load_library().sparvar_map_index(geom.ref, S, k, B, H, topk, _ptr(topk_idx), _ptr(local_row_ptr),
                                             _ptr(local_col_idx), radius, prev_dilation, _ptr(row_ptr),
                                             _ptr(col_idx), col_idx.numel(), _ptr(schedule), _stream(stream)))

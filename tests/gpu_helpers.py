@@ -40,10 +40,20 @@ def to_dev(x, dtype):
     return torch.from_numpy(np.ascontiguousarray(x)).to("cuda").to(torch_dtype(dtype))
 
 
-def csr_rows(row_ptr, col_idx):
+def csr_rows(row_ptr, col_idx, padded=False):
+    """Rows of a CSR pair; with padded=True, drop the -1 entries that end each row
+    (after checking that -1 only appears as trailing padding)."""
     rp = row_ptr.cpu().numpy().astype(np.int64)
     ci = col_idx.cpu().numpy().astype(np.int64)
-    return [ci[rp[i]:rp[i + 1]].tolist() for i in range(len(rp) - 1)]
+    rows = [ci[rp[i]:rp[i + 1]].tolist() for i in range(len(rp) - 1)]
+    if padded:
+        out = []
+        for r in rows:
+            n = len(r) - (r[::-1].index(next(x for x in r[::-1] if x != -1)) if any(x != -1 for x in r) else len(r))
+            assert all(x == -1 for x in r[n:]) and all(x != -1 for x in r[:n]), r
+            out.append(r[:n])
+        rows = out
+    return rows
 
 
 def assert_close(got, want, dtype, what):

@@ -60,7 +60,9 @@ def test_local_capacity_matches_oracle():
 def test_map_capacity_bound():
     g = sv.Geometry(INF, INF, 8, 4)
     rows = o_local_blocks(OGeom(INF, INF, 8, 4), 13, 1)
-    assert sv.sparvar_map_index_capacity(g, 10, 13, 2, 16, 8, 1) == 2 * 16 * 64 * (max(map(len, rows)) + 8)
+    # every row at its longest (local + top-k), plus one length slot per row
+    rows_n = 2 * 16 * 64
+    assert sv.sparvar_map_index_capacity(g, 10, 13, 2, 16, 8, 1) == rows_n * (max(map(len, rows)) + 8) + rows_n
 
 
 @pytest.mark.parametrize("args,status", [

@@ -27,7 +27,8 @@ def run_case(h, w, b, ns, S, steps, B, H, d, F, topk, r, dtype, seed=0, dil=0, h
     Qd, Kd, Vd = to_dev(q, dtype), to_dev(k, dtype), to_dev(v, dtype)
     g = sv.Geometry(h, w, b, ns)
     og = oracle_geometry(h, w, b, ns)
-    path = SparsePath(g, S, steps, B, H, d, topk, r, dil, dtype=torch_dtype(dtype), use_schedule=True)
+    path = SparsePath(g, S, steps, B, H, d, topk, r, dil, dtype=torch_dtype(dtype), use_schedule=True,
+                      local_lists=True)
     path.build_local()
     path.decision(Qd, Kd, Vd)
     lse_k = {}
@@ -70,10 +71,19 @@ def run_case(h, w, b, ns, S, steps, B, H, d, F, topk, r, dtype, seed=0, dil=0, h
         # merged rows: bit-exact
         rows = O.build_rows(og, S, kk, tk, loc)
         rp, ci, sch = path.csr[kk]
-        got = csr_rows(rp, ci)
+        got = csr_rows(rp, ci, padded=True)
         assert got == [r_ for per in rows for r_ in per], f"CSR rows step {kk}"
+        stride = rp[1].item() - rp[0].item()
+        assert (np.diff(rp.cpu().numpy()) == stride).all()
+        # the mapping call generating the local rows itself gives the same rows
+        path.local_lists = False
+        path.map_step(kk)
+        torch.cuda.synchronize()
+        assert csr_rows(rp, ci, padded=True) == got, f"CSR rows (in-call local rows) step {kk}"
+        path.local_lists = True
         if check_schedule and sch is not None:
-            assert sch.cpu().numpy().tolist() == O.longest_first(rp.cpu().numpy()), f"schedule step {kk}"
+            compact_ptr, _ = O.rows_to_csr(got)
+            assert sch.cpu().numpy().tolist() == O.longest_first(compact_ptr), f"schedule step {kk}"
         # attention
         ok = path.out[kk].float().cpu().numpy().reshape(BH, -1, d)
         lk = lse_k[kk].cpu().numpy().reshape(BH, -1)
@@ -102,7 +112,7 @@ def test_tiny_config_every_block_kept(dtype):
     q, k, v = make_case(h, h, 1, 1, 64, 8, 2, 0, dtype)
     o_ref, _ = O.dense_attention(q[0, 0, og.C(3):og.C(4)], k[0, 0], v[0, 0], scale_of(64))
     assert_close(path.out[4].float().cpu().numpy()[0, 0], o_ref, dtype, "sparse == dense")
-    assert all(len(r) == 7 for r in csr_rows(*path.csr[4][:2]))
+    assert all(len(r) == 7 for r in csr_rows(*path.csr[4][:2], padded=True))
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
