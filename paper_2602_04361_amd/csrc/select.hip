@@ -1,9 +1,9 @@
 // Decision-scale block selection (Sec. 3.2: column-sum D and TopK).
 //
-// pooled_scores_kernel: one workgroup per (b, h, query tile g of scale S).
-//   For every block v of scales 1..S it recomputes the S^T = K Q^T tile with
-//   MFMA and adds P = exp(scale * s - lse) over the tile's queries and the
-//   block's keys. Sums run in a fixed order (lane, shuffle tree, waves in
+// pooled_scores_kernel: one workgroup per (b, h, group of query tiles of
+//   scale S). For every block v of scales 1..S it recomputes the S^T = K Q^T
+//   tile with MFMA and adds P = exp(scale * s - lse) over each tile's queries and
+//   the block's keys. Sums run in a fixed order (lane, shuffle tree, waves in
 //   order), so results are deterministic.
 // topk_kernel: one wave per (b, h, g) row; candidate v is kept iff fewer than
 //   topk candidates beat it (higher score, or equal score and lower id); kept
@@ -138,31 +138,38 @@ struct BlockWalker {
   }
 };
 
-// bf16 scoring: one workgroup per (b, h, query tile g of scale S). K chunks stream
-// HBM -> LDS (direct 16-byte loads, swizzled rows, double buffered); S^T = K Q^T
-// on MFMA; each lane accumulates exp2(scale*log2e*s - lse*log2e) over its keys
-// and its query; at the end of a block the wave sum goes to LDS, and the final
-// score is the sum over waves in order (deterministic).
-template <int D, int NW>
-__global__ __launch_bounds__(NW * 64) void pooled_scores_kernel(ScoreIO io) {
+// bf16 scoring: one workgroup per (b, h, group of TPW query tiles of scale S),
+// WPT waves per tile. Every query of a head scores against all keys of scales
+// 1..S, so the tiles of a group share each K chunk: chunks stream HBM -> LDS
+// (direct 16-byte loads, swizzled rows, double buffered) once per group.
+// S^T = K Q^T on MFMA; each lane accumulates exp2(scale*log2e*s - lse*log2e) over
+// its keys and its query; at the end of a block the wave sum goes to LDS, and a
+// tile's score is the sum over its waves in order (deterministic). Blocks of a
+// row are split over grid.y.
+template <int D, int WPT, int TPW>
+__global__ __launch_bounds__(WPT * TPW * 64) void pooled_scores_kernel(ScoreIO io) {
+  constexpr int NW = WPT * TPW;
   constexpr int KC = 64, NT = NW * 64, U = D / 8, kRow = D * 2, kTile = KC * kRow;
   constexpr int kLoads = KC * U / NT;
   static_assert((KC * U) % NT == 0, "chunk must split evenly over the workgroup");
   __shared__ __attribute__((aligned(16))) char smem[2 * kTile];
-  extern __shared__ float red[];  // [NW][NB] per-wave block sums
+  extern __shared__ float red[];  // [NW][per] per-wave block sums
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, half = lane >> 5;
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
-  const int32_t row = blockIdx.x;  // (b*H + h) * G_S + g
-  const int32_t bh = row / io.G_S, g = row - bh * io.G_S;
+  const int32_t groups = (io.G_S + TPW - 1) / TPW;
+  const int32_t bh = blockIdx.x / groups;
+  const int32_t g0 = (blockIdx.x - bh * groups) * TPW;
   const GeoTable& G = io.G;
   const int S = io.S;
   const int32_t tw = G.Tw[S - 1];
-  const Tile qt = tile_at(G, S, g / tw, g % tw);
+  const int32_t g = g0 + wave / WPT;  // this wave's query tile
+  const bool gvalid = g < io.G_S;
+  const Tile qt = tile_at(G, S, gvalid ? g / tw : 0, gvalid ? g % tw : 0);
   const int32_t nq = qt.nr * qt.nc;
-  const int32_t qslot = wave * kQPerWave + l32;
-  const bool qvalid = qslot < nq;
+  const int32_t qslot = (wave % WPT) * kQPerWave + l32;
+  const bool qvalid = gvalid && qslot < nq;
   const int32_t qi = qvalid ? qslot : 0;
   const int32_t qrow = (qt.base - G.C[S - 1]) + (qi / qt.nc) * qt.stride + (qi % qt.nc);
   const bf16_bits* qplane = static_cast<const bf16_bits*>(io.q) + (int64_t)bh * io.q_bh_stride;
@@ -241,10 +248,8 @@ __global__ __launch_bounds__(NW * 64) void pooled_scores_kernel(ScoreIO io) {
     }
     psum += qvalid ? part : 0.f;
     if (last0) {
-      float s = psum;
-#pragma unroll
-      for (int off = 32; off >= 1; off >>= 1) s += __shfl_xor(s, off, 64);
-      if (lane == 0) red[wave * per + (b0 - v0)] = s;
+      const float sw = wave_sum(psum);
+      if (lane == 0) red[wave * per + (b0 - v0)] = sw;
       psum = 0.f;
     }
     c0 = cn;
@@ -257,12 +262,15 @@ __global__ __launch_bounds__(NW * 64) void pooled_scores_kernel(ScoreIO io) {
     if (!step(std::integral_constant<int, 1>{})) break;
   }
   __syncthreads();
-  float* out = io.scores + (int64_t)row * io.NB;
-  for (int32_t v = v0 + tid; v < v1; v += NT) {
+  const int32_t nv = v1 - v0;
+  for (int32_t i = tid; i < TPW * nv; i += NT) {
+    const int t = i / nv;
+    const int32_t v = v0 + (i - t * nv);
+    if (g0 + t >= io.G_S) continue;
     float sc = 0.f;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) sc += red[w * per + (v - v0)];
-    out[v] = sc;
+    for (int w = 0; w < WPT; ++w) sc += red[(t * WPT + w) * per + (v - v0)];
+    io.scores[((int64_t)bh * io.G_S + g0 + t) * io.NB + v] = sc;
   }
 }
 
@@ -308,25 +316,31 @@ hipError_t launch_scores_f32(const ScoreIO& io, int nw, int32_t grid, hipStream_
   }
   return hipGetLastError();
 }
-// Blocks of a row are split over grid.y so that about 2048 workgroups run.
-template <int D>
-hipError_t launch_scores_bf16(const ScoreIO& io, int nw, int32_t grid, hipStream_t stream) {
-  int32_t splits = (2048 + grid - 1) / grid;
+// Query tiles of a head are grouped (TPW per workgroup) and the blocks of a row
+// split over grid.y so that about 1024 workgroups run.
+template <int D, int WPT, int TPW>
+hipError_t launch_scores_bf16(const ScoreIO& io, int32_t BH, hipStream_t stream) {
+  const int32_t grid = BH * ((io.G_S + TPW - 1) / TPW);
+  int32_t splits = (1024 + grid - 1) / grid;
   if (splits > io.NB) splits = io.NB;
   if (splits < 1) splits = 1;
   const int32_t per = (io.NB + splits - 1) / splits;
   splits = (io.NB + per - 1) / per;
   ScoreIO io2 = io;
   io2.per = per;
-  const size_t red = (size_t)nw * per * sizeof(float);
-  const dim3 g(grid, splits);
-  switch (nw) {
-    case 1: hipLaunchKernelGGL((pooled_scores_kernel<D, 1>), g, dim3(64), red, stream, io2); break;
-    case 2: hipLaunchKernelGGL((pooled_scores_kernel<D, 2>), g, dim3(128), red, stream, io2); break;
-    case 4: hipLaunchKernelGGL((pooled_scores_kernel<D, 4>), g, dim3(256), red, stream, io2); break;
-    default: hipLaunchKernelGGL((pooled_scores_kernel<D, 8>), g, dim3(512), red, stream, io2); break;
-  }
+  const size_t red = (size_t)WPT * TPW * per * sizeof(float);
+  hipLaunchKernelGGL((pooled_scores_kernel<D, WPT, TPW>), dim3(grid, splits), dim3(WPT * TPW * 64), red, stream, io2);
   return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_scores_bf16_d(const ScoreIO& io, int32_t BH, int wpt, hipStream_t stream) {
+  switch (wpt) {
+    case 1: return launch_scores_bf16<D, 1, 4>(io, BH, stream);
+    case 2: return launch_scores_bf16<D, 2, 4>(io, BH, stream);
+    case 4: return launch_scores_bf16<D, 4, 1>(io, BH, stream);
+    default: return launch_scores_bf16<D, 8, 1>(io, BH, stream);
+  }
 }
 }  // namespace
 
@@ -350,8 +364,9 @@ hipError_t launch_pooled_scores(const ScoreArgs& a, hipStream_t stream) {
   const int nw = tile_q <= 32 ? 1 : tile_q <= 64 ? 2 : tile_q <= 128 ? 4 : 8;
   const int32_t grid = a.BH * io.G_S;
   if (grid == 0) return hipSuccess;
-  if (a.bf16 && (size_t)nw * io.NB * sizeof(float) <= 32 * 1024)
-    return a.d == 64 ? launch_scores_bf16<64>(io, nw, grid, stream) : launch_scores_bf16<128>(io, nw, grid, stream);
+  // per-wave block sums in LDS: at most 8 waves x NB floats
+  if (a.bf16 && (size_t)8 * io.NB * sizeof(float) <= 32 * 1024)
+    return a.d == 64 ? launch_scores_bf16_d<64>(io, a.BH, nw, stream) : launch_scores_bf16_d<128>(io, a.BH, nw, stream);
   if (a.bf16) return a.d == 64 ? launch_scores_f32<bf16_bits, 64>(io, nw, grid, stream)
                                : launch_scores_f32<bf16_bits, 128>(io, nw, grid, stream);
   return a.d == 64 ? launch_scores_f32<float, 64>(io, nw, grid, stream) : launch_scores_f32<float, 128>(io, nw, grid, stream);
