@@ -39,11 +39,13 @@ N_SETS = 4
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--sets", type=int, default=N_SETS)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="finish with three plain device copies of 256 MiB (reference for HBM byte counters)")
     return ap.parse_args()
 
 
@@ -248,9 +250,13 @@ def main():
     end.record(stream)
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
+    step_ms = np.array([evs[i][0].elapsed_time(evs[i][-1]) for i in range(args.steps)])
     ms_step = total_ms / args.steps
-    per = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(args.steps)]))
-           for j, n in enumerate(names)}
+    samples = {n: np.array([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(args.steps)])
+               for j, n in enumerate(names)}
+    per = {n: float(np.mean(x)) for n, x in samples.items()}
+    spread = {n: {"median": float(np.median(x)), "p10": float(np.percentile(x, 10)), "p90": float(np.percentile(x, 90))}
+              for n, x in samples.items()}
 
     # our dense kernel at the 64x64 step (speedup denominator), same buffers and rotation
     i13 = info[13]
@@ -278,11 +284,14 @@ def main():
         "dense_S": {"ms": per["dense_S"], "tflops": dense_S_flops / per["dense_S"] / 1e9},
         "select": {"ms": per["select"], "tflops": score_flops / per["select"] / 1e9},
     }
+    for n in ("dense_S", "select"):
+        kernels[n].update({"ms_" + q: v for q, v in spread[n].items()})
     for kk in CFG["steps"]:
         f, b_, dens, keys = acct[kk]
         side = info[kk]["h"]
-        kernels[f"map_{side}"] = {"ms": per[f"map_{kk}"]}
-        kernels[f"attn_{side}"] = {"ms": per[f"attn_{kk}"], "gflop": f / 1e9,
+        kernels[f"map_{side}"] = {"ms": per[f"map_{kk}"], **{"ms_" + q: v for q, v in spread[f"map_{kk}"].items()}}
+        kernels[f"attn_{side}"] = {"ms": per[f"attn_{kk}"], **{"ms_" + q: v for q, v in spread[f"attn_{kk}"].items()},
+                                   "gflop": f / 1e9,
                                    "tflops": f / per[f"attn_{kk}"] / 1e9,
                                    "frac_bf16_peak": f / per[f"attn_{kk}"] / 1e9 / PEAK_BF16_TFLOPS,
                                    "hbm_gbs_algorithmic": b_ / per[f"attn_{kk}"] / 1e6,
@@ -294,6 +303,17 @@ def main():
                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                 "traffic": traffic, "algorithmic_bytes": b13, "algorithmic_flops": f13,
                 "dominant_kernel_in_step": dominant}
+
+    if args.copy_calibration:
+        # plain device copies of known size: the reference that scales the HBM byte
+        # counters (FETCH_SIZE, WRITE_SIZE) of the kernels above
+        src = torch.ones(64 << 20, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(f"[bench] copy calibration: 3 x {src.numel() * 4} bytes read and written", file=sys.stderr, flush=True)
+        del src, dst
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -317,6 +337,8 @@ def main():
                    "block": "8x8 tokens", "topk": CFG["topk"], "window_radius": CFG["radius"],
                    "sink_scales": CFG["n_sink"], "kv_tokens_last_step": info[13]["n_tokens_le"]},
         "ms_per_layer": ms_step,
+        "ms_per_step_spread": {"median": float(np.median(step_ms)), "p10": float(np.percentile(step_ms, 10)),
+                               "p90": float(np.percentile(step_ms, 90))},
         "sparse_64": {"ms": attn13_ms, "tflops": achieved, "frac_bf16_peak": achieved / PEAK_BF16_TFLOPS,
                       "density": dens13, "dense_ms": dense64_ms,
                       "dense_tflops": dense64_flops / dense64_ms / 1e9,

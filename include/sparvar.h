@@ -191,10 +191,14 @@ int sparvar_map_index(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t
  *   q_k: [B,H,N_k,d] (plane stride q_bh_stride); k_lek, v_lek: [B,H,N_<=k,d]
  *   (plane stride kv_bh_stride); o: [B,H,N_k,d] contiguous; lse (nullable):
  *   [B,H,N_k] fp32. A row with no valid block yields o = 0, lse = -inf.
- *   row_ptr / col_idx: CSR over B*H*G_k rows with ascending block ids
- *   (as written by sparvar_map_index); ids outside [0, NB_<=k) are skipped.
- *   schedule (nullable): a permutation of the rows giving the launch order;
- *   it changes only the order of work, never the results.
+ *   row_ptr / col_idx: CSR over B*H*G_k rows; ids outside [0, NB_<=k) are
+ *   skipped wherever they appear, and the remaining ids of a row must be
+ *   strictly ascending (as written by sparvar_map_index). A row that repeats
+ *   an id or lists ids out of order gives unspecified values (never an access
+ *   outside the inputs and outputs).
+ *   schedule (nullable): a permutation of the rows giving the launch order
+ *   of the one-tile-per-workgroup form; it changes only the order of work,
+ *   never the results (the form that groups neighbouring tiles ignores it).
  */
 int sparvar_block_sparse_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t B, int32_t H,
                                   int32_t d, sparvar_dtype_t dtype, const void* q_k,

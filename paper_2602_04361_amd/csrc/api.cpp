@@ -1,6 +1,7 @@
 // C ABI entry points: host-side validation, geometry tables, launches.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -33,6 +34,20 @@ int ok() {
 int hip_status(hipError_t e, const char* what) {
   if (e == hipSuccess) return ok();
   return fail(SPARVAR_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Compute units of the current device (queried once per device; concurrent
+// first calls store the same value).
+int device_cus() {
+  static std::atomic<int> cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n <= 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cached[dev].store(n, std::memory_order_relaxed);
+  }
+  return n;
 }
 
 // Env knobs for launch shape experiments (defaults are the tuned choice).
@@ -344,6 +359,10 @@ int sparvar_block_sparse_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_
   a.chunk = env_int("SPARVAR_SPARSE_CHUNK", 32);
   a.stages = env_int("SPARVAR_SPARSE_STAGES", 2);
   a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
+  a.group_waves = env_int("SPARVAR_SPARSE_GROUP_WAVES", -1);
+  a.group_chunk = env_int("SPARVAR_SPARSE_GROUP_CHUNK", 64);
+  a.group_stages = env_int("SPARVAR_SPARSE_GROUP_STAGES", 2);
+  a.num_cu = device_cus();
   return hip_status(launch_sparse_attn(a, stream), "block-sparse attention launch");
 }
 

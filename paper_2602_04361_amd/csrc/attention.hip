@@ -59,16 +59,21 @@ struct DenseCursor {
 template <int KC>
 struct DenseSrc {
   static constexpr bool kSparse = false;
+  static constexpr bool kGrouped = false;
   int32_t n_q, n_kv, slabs, q_per_wg;
-  __device__ __forceinline__ QuerySet queries(int32_t item) const {
+  template <int NT>
+  static constexpr int table_bytes() { return 16; }
+  __device__ __forceinline__ int tile_of(int) const { return 0; }
+  __device__ __forceinline__ QuerySet queries(int32_t item, int wave) const {
     QuerySet s;
     s.bh = item / slabs;
     const int32_t slab = item - s.bh * slabs;
     s.qbase = 0;
     s.qnc = n_q;
     s.qstride = 0;
-    s.q0 = slab * q_per_wg;
-    s.q1 = (s.q0 + q_per_wg < n_q) ? s.q0 + q_per_wg : n_q;
+    const int32_t q0 = slab * q_per_wg;
+    s.q1 = (q0 + q_per_wg < n_q) ? q0 + q_per_wg : n_q;
+    s.q0 = q0 + wave * kQPerWave;
     return s;
   }
   __device__ __forceinline__ DenseCursor<KC> cursor(int32_t) const { return DenseCursor<KC>{0, n_kv}; }
@@ -147,22 +152,35 @@ struct CsrCursor {
   }
 };
 
-// Chunk list of one CSR row, decoded in parallel by the whole workgroup into an
+// Chunk list of a block list, decoded in parallel by the whole workgroup into an
 // LDS table: each refill decodes up to `group` blocks (one per thread), merges
-// runs of contiguous blocks, splits everything into chunks of at most KC keys
-// and writes 8-byte descriptors; the main loop then only reads descriptors.
-// Descriptor: x = first token, y = stride << 16 | nc << 8 | count.
+// runs of contiguous blocks that have the same tile mask, splits everything into
+// chunks of at most KC keys and writes 8-byte descriptors plus the mask; the main
+// loop then only reads descriptors. Descriptor: x = first token,
+// y = stride << 16 | nc << 8 | count.
+// Blocks supplies the ids: id(i) and mask(i) for i in the current segment
+// [pos, end), and segment(pos, end), which moves to the next segment (false when
+// there is none). Every thread of the workgroup calls next() in the same order.
 constexpr int kTableCap = 256;
 
-template <int KC, int NT>
+template <int NT>
+struct TableLds {  // byte offsets inside the table region
+  static constexpr int kTbl = 0;
+  static constexpr int kTmask = kTbl + kTableCap * 8;
+  static constexpr int kInfo = kTmask + kTableCap * 4;
+  static constexpr int kImask = kInfo + NT * 16;
+  static constexpr int kWt = kImask + NT * 4;
+  static constexpr int kBytes = kWt + 16 * 4;
+};
+
+template <int KC, int NT, class Blocks>
 struct TableCursor {
   const GeoTable* G;
-  const int32_t* __restrict__ col;
-  int32_t pos, end, nb, group;
-  int32_t tn, ti;
-  uint2* tbl;    // [kTableCap]
-  int4* info;    // [NT] decoded tiles of the current group (nr = 0: skipped id)
-  int32_t* cnt;  // [NT + 1] chunk counts, then exclusive offsets
+  Blocks blocks;
+  int32_t nb, group;
+  int32_t pos, end;  // entries of the current segment not yet decoded
+  int32_t tn, ti;    // table fill and read position
+  char* lds;         // TableLds<NT> region
 
   __device__ __forceinline__ static bool contiguous(const int4& x) { return x.y == 1 || x.z == x.w; }
 
@@ -175,36 +193,45 @@ struct TableCursor {
     return x.y * ((x.z + KC - 1) / KC);
   }
 
-  __device__ void refill() {
+  __device__ __forceinline__ void refill() {
+    using L = TableLds<NT>;
+    uint2* tbl = reinterpret_cast<uint2*>(lds + L::kTbl);
+    uint32_t* tmask = reinterpret_cast<uint32_t*>(lds + L::kTmask);
+    int4* info = reinterpret_cast<int4*>(lds + L::kInfo);
+    uint32_t* imask = reinterpret_cast<uint32_t*>(lds + L::kImask);
+    int32_t* wt = reinterpret_cast<int32_t*>(lds + L::kWt);
     const int tid = threadIdx.x;
     __syncthreads();
     const int32_t nblk = (end - pos < group) ? end - pos : group;
     if (tid < nblk) {
-      const int32_t v = col[pos + tid];
+      const int32_t v = blocks.id(pos + tid);
       int4 x = make_int4(0, 0, 1, 1);
       if (v >= 0 && v < nb) {
         const Tile t = block_tile(*G, v);
         x = make_int4(t.base, t.nr, t.nc, t.stride);
       }
       info[tid] = x;
+      imask[tid] = blocks.mask(pos + tid);
     }
     __syncthreads();
     int32_t n = 0, run_total = 0;
     int4 x = make_int4(0, 0, 1, 1);
+    uint32_t m = 0;
     if (tid < nblk) {
       x = info[tid];
+      m = imask[tid];
       if (x.y > 0) {
         bool cont = false;
         if (contiguous(x) && tid > 0) {
           const int4 p = info[tid - 1];
-          cont = p.y > 0 && contiguous(p) && p.x + p.y * p.z == x.x;
+          cont = p.y > 0 && contiguous(p) && p.x + p.y * p.z == x.x && imask[tid - 1] == m;
         }
         if (!cont) {
           run_total = x.y * x.z;
           if (contiguous(x)) {
             for (int32_t u = tid + 1; u < nblk; ++u) {
               const int4 y = info[u];
-              if (y.y > 0 && contiguous(y) && y.x == x.x + run_total) run_total += y.y * y.z;
+              if (y.y > 0 && contiguous(y) && y.x == x.x + run_total && imask[u] == m) run_total += y.y * y.z;
               else break;
             }
           }
@@ -212,35 +239,28 @@ struct TableCursor {
         }
       }
     }
-    // exclusive scan of n over the workgroup
-    cnt[tid] = n;
-    __syncthreads();
-    for (int off = 1; off < NT; off <<= 1) {
-      const int32_t add = tid >= off ? cnt[tid - off] : 0;
-      __syncthreads();
-      cnt[tid] += add;
-      __syncthreads();
-    }
-    const int32_t incl = cnt[tid];
-    const int32_t total = cnt[NT - 1];
-    int32_t o = incl - n;
+    int32_t total;
+    int32_t o = block_excl_scan<NT>(n, wt, total);
     if (n > 0) {
       if (contiguous(x)) {
         for (int32_t done = 0; done < run_total; done += KC, ++o) {
-          const int32_t m = (run_total - done < KC) ? run_total - done : KC;
-          tbl[o] = make_uint2((uint32_t)(x.x + done), (uint32_t)((kChunk << 16) | (kChunk << 8) | m));
+          const int32_t cnt = (run_total - done < KC) ? run_total - done : KC;
+          tbl[o] = make_uint2((uint32_t)(x.x + done), (uint32_t)((kChunk << 16) | (kChunk << 8) | cnt));
+          tmask[o] = m;
         }
       } else if (x.z <= KC) {
         const int32_t rpc = KC / x.z;
         for (int32_t r0 = 0; r0 < x.y; r0 += rpc, ++o) {
           const int32_t rows = (x.y - r0 < rpc) ? x.y - r0 : rpc;
           tbl[o] = make_uint2((uint32_t)(x.x + r0 * x.w), (uint32_t)((x.w << 16) | (x.z << 8) | (rows * x.z)));
+          tmask[o] = m;
         }
       } else {
         for (int32_t r0 = 0; r0 < x.y; ++r0)
           for (int32_t c0 = 0; c0 < x.z; c0 += KC, ++o) {
-            const int32_t m = (x.z - c0 < KC) ? x.z - c0 : KC;
-            tbl[o] = make_uint2((uint32_t)(x.x + r0 * x.w + c0), (uint32_t)((kChunk << 16) | (kChunk << 8) | m));
+            const int32_t cnt = (x.z - c0 < KC) ? x.z - c0 : KC;
+            tbl[o] = make_uint2((uint32_t)(x.x + r0 * x.w + c0), (uint32_t)((kChunk << 16) | (kChunk << 8) | cnt));
+            tmask[o] = m;
           }
       }
     }
@@ -251,17 +271,40 @@ struct TableCursor {
   }
 
   __device__ __forceinline__ bool next(Chunk& c) {
+    using L = TableLds<NT>;
     while (ti >= tn) {
-      if (pos >= end) return false;
+      if (pos >= end) {
+        if (!blocks.segment(pos, end)) return false;
+        continue;
+      }
       refill();
     }
-    const uint2 e = tbl[ti++];
+    const uint2 e = reinterpret_cast<const uint2*>(lds + L::kTbl)[ti];
+    const uint32_t m = reinterpret_cast<const uint32_t*>(lds + L::kTmask)[ti];
+    ++ti;
     const uint32_t y = __builtin_amdgcn_readfirstlane(e.y);
     c.base = __builtin_amdgcn_readfirstlane(e.x);
     c.stride = (int32_t)(y >> 16);
     c.nc = (int32_t)((y >> 8) & 0xff);
     c.count = (int32_t)(y & 0xff);
     c.magic = kNcMagic[c.nc];
+    c.mask = __builtin_amdgcn_readfirstlane(m);
+    return true;
+  }
+};
+
+// Block list of one CSR row in global memory (a single segment, every tile).
+struct CsrBlocks {
+  const int32_t* __restrict__ col;
+  int32_t p0, p1;
+  bool done;
+  __device__ __forceinline__ int32_t id(int32_t i) const { return col[i]; }
+  __device__ __forceinline__ uint32_t mask(int32_t) const { return ~0u; }
+  __device__ __forceinline__ bool segment(int32_t& pos, int32_t& end) {
+    if (done) return false;
+    done = true;
+    pos = p0;
+    end = p1;
     return true;
   }
 };
@@ -269,6 +312,7 @@ struct TableCursor {
 template <int KC>
 struct SparseSrc {
   static constexpr bool kSparse = true;
+  static constexpr bool kGrouped = false;
   GeoTable G;
   const int32_t* row_ptr;
   const int32_t* col_idx;
@@ -276,11 +320,14 @@ struct SparseSrc {
   int32_t k, G_k, slabs, q_per_wg;
   int32_t max_chunks_per_block;  // bound used to size a table refill
 
+  template <int NT>
+  static constexpr int table_bytes() { return TableLds<NT>::kBytes; }
+  __device__ __forceinline__ int tile_of(int) const { return 0; }
   __device__ __forceinline__ int32_t row_of(int32_t item) const {
     const int32_t r = item / slabs;
     return schedule ? schedule[r] : r;
   }
-  __device__ __forceinline__ QuerySet queries(int32_t item) const {
+  __device__ __forceinline__ QuerySet queries(int32_t item, int wave) const {
     const int32_t r = row_of(item);
     const int32_t slab = item - (item / slabs) * slabs;
     QuerySet s;
@@ -292,8 +339,9 @@ struct SparseSrc {
     s.qnc = t.nc;
     s.qstride = t.stride;
     const int32_t nq = t.nr * t.nc;
-    s.q0 = slab * q_per_wg;
-    s.q1 = (s.q0 + q_per_wg < nq) ? s.q0 + q_per_wg : nq;
+    const int32_t q0 = slab * q_per_wg;
+    s.q1 = (q0 + q_per_wg < nq) ? q0 + q_per_wg : nq;
+    s.q0 = q0 + wave * kQPerWave;
     return s;
   }
   __device__ __forceinline__ CsrCursor<KC> cursor(int32_t item) const {
@@ -312,23 +360,264 @@ struct SparseSrc {
     return c;
   }
   template <int NT>
-  __device__ __forceinline__ TableCursor<KC, NT> table_cursor(int32_t item, uint2* tbl, int4* info,
-                                                              int32_t* cnt) const {
+  __device__ __forceinline__ TableCursor<KC, NT, CsrBlocks> table_cursor(int32_t item, char* lds) const {
     const int32_t r = row_of(item);
-    TableCursor<KC, NT> c;
+    TableCursor<KC, NT, CsrBlocks> c;
     c.G = &G;
-    c.col = col_idx;
-    c.pos = row_ptr[r];
-    c.end = row_ptr[r + 1];
+    c.blocks.col = col_idx;
+    c.blocks.p0 = row_ptr[r];
+    c.blocks.p1 = row_ptr[r + 1];
+    c.blocks.done = false;
     c.nb = G.NB[k];
     const int32_t g = kTableCap / (max_chunks_per_block > 0 ? max_chunks_per_block : 1);
     c.group = g < NT ? (g > 0 ? g : 1) : NT;
+    c.pos = 0;
+    c.end = 0;
     c.tn = 0;
     c.ti = 0;
-    c.tbl = tbl;
-    c.info = info;
-    c.cnt = cnt;
+    c.lds = lds;
     return c;
+  }
+};
+
+// ------------------------------------------------------- grouped query tiles
+// A workgroup serves a group of T neighbouring query tiles of scale k (T = 2,
+// 4 or 8; gh x gw tiles) and walks the union of their CSR rows once: every
+// staged chunk carries the mask of the group's tiles whose row lists the block,
+// and the waves of the other tiles skip it. Each tile still attends to exactly
+// its own blocks; the union only lets tiles share each HBM -> LDS copy.
+//
+// Union of sorted rows, built in parallel (thread = row entry): each row's
+// valid ids are compacted; an entry is the owner of its id when no lower row and
+// no earlier entry of its own row holds the id; its place in the union is the
+// number of owners with smaller ids, found by a binary search in every other
+// row; its mask has a bit for every row holding the id. Rows longer than
+// NT / T entries are served tile by tile instead, in windows of NT entries.
+template <int NT>
+struct GroupLds {
+  static constexpr int kIds = 0;
+  static constexpr int kOwnp = kIds + NT * 4;
+  static constexpr int kUid = kOwnp + NT * 4;
+  static constexpr int kUmask = kUid + NT * 4;
+  static constexpr int kRowP = kUmask + NT * 4;
+  static constexpr int kRowN = kRowP + 8 * 4;
+  static constexpr int kRowC = kRowN + 8 * 4;
+  static constexpr int kWt = kRowC + 8 * 4;
+  static constexpr int kBytes = kWt + 16 * 4;
+};
+
+template <int NT>
+struct GroupBlocks {
+  static constexpr int kLgNT = NT == 512 ? 9 : NT == 256 ? 8 : NT == 128 ? 7 : 6;
+  const int32_t* __restrict__ col;
+  int32_t nb, T, lgT;
+  bool by_tile, started;
+  int32_t seg_t, seg_off;  // next window of the tile-by-tile mode
+  char* lds;               // GroupLds<NT> region
+
+  __device__ __forceinline__ int32_t* arr(int off) const { return reinterpret_cast<int32_t*>(lds + off); }
+  __device__ __forceinline__ int32_t id(int32_t i) const { return arr(GroupLds<NT>::kUid)[i]; }
+  __device__ __forceinline__ uint32_t mask(int32_t i) const {
+    return (uint32_t)arr(GroupLds<NT>::kUmask)[i];
+  }
+
+  __device__ __forceinline__ int32_t build_union() {
+    using L = GroupLds<NT>;
+    int32_t* ids = arr(L::kIds);
+    int32_t* ownp = arr(L::kOwnp);
+    const int32_t* rowp = arr(L::kRowP);
+    const int32_t* rown = arr(L::kRowN);
+    int32_t* rowc = arr(L::kRowC);
+    int32_t* wt = arr(L::kWt);
+    const int tid = threadIdx.x;
+    const int lgRC = kLgNT - lgT;
+    const int32_t RC = 1 << lgRC;
+    const int t = tid >> lgRC;
+    const int32_t i = tid & (RC - 1);
+    int32_t raw = -1;
+    if (i < rown[t]) raw = col[rowp[t] + i];
+    const bool valid = raw >= 0 && raw < nb;
+    int32_t total;
+    const int32_t e = block_excl_scan<NT>(valid ? 1 : 0, wt, total);
+    ownp[tid] = e;
+    __syncthreads();
+    const int32_t row0 = ownp[t * RC];
+    if (valid) ids[t * RC + (e - row0)] = raw;
+    if (i == 0) rowc[t] = ((t + 1) * RC < NT ? ownp[(t + 1) * RC] : total) - row0;
+    __syncthreads();
+
+    const int32_t nt = rowc[t];
+    int32_t v = 0;
+    uint32_t m = 0;
+    bool own = false;
+    if (i < nt) {
+      v = ids[t * RC + i];
+      own = !(i > 0 && ids[t * RC + i - 1] == v);
+      m = 1u << t;
+    }
+    int32_t lb[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      lb[u] = 0;
+      if (u < T && i < nt) {
+        if (u == t) {
+          lb[u] = i;
+        } else {
+          const int32_t* r = ids + u * RC;
+          const int32_t n = rowc[u];
+          int32_t lo = 0, hi = n;
+          while (lo < hi) {
+            const int32_t mid = (lo + hi) >> 1;
+            if (r[mid] < v) lo = mid + 1;
+            else hi = mid;
+          }
+          lb[u] = lo;
+          if (lo < n && r[lo] == v) {
+            m |= 1u << u;
+            if (u < t) own = false;
+          }
+        }
+      }
+    }
+    int32_t owners;
+    const int32_t e2 = block_excl_scan<NT>(own ? 1 : 0, wt, owners);
+    ownp[tid] = e2;
+    __syncthreads();
+    if (own) {
+      int32_t rank = 0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (u < T) {
+          const int32_t base = ownp[u * RC];
+          const int32_t j = lb[u];
+          const int32_t at = j < RC ? ownp[u * RC + j] : ((u + 1) * RC < NT ? ownp[(u + 1) * RC] : owners);
+          rank += at - base;
+        }
+      }
+      arr(L::kUid)[rank] = v;
+      arr(L::kUmask)[rank] = (int32_t)m;
+    }
+    __syncthreads();
+    return __builtin_amdgcn_readfirstlane(owners);
+  }
+
+  __device__ __forceinline__ int32_t build_window() {
+    using L = GroupLds<NT>;
+    const int tid = threadIdx.x;
+    const int32_t n = arr(L::kRowN)[seg_t] - seg_off;
+    int32_t raw = -1;
+    if (tid < n) raw = col[arr(L::kRowP)[seg_t] + seg_off + tid];
+    const bool valid = raw >= 0 && raw < nb;
+    int32_t total;
+    const int32_t e = block_excl_scan<NT>(valid ? 1 : 0, arr(L::kWt), total);
+    if (valid) {
+      arr(L::kUid)[e] = raw;
+      arr(L::kUmask)[e] = 1 << seg_t;
+    }
+    __syncthreads();
+    return __builtin_amdgcn_readfirstlane(total);
+  }
+
+  __device__ __forceinline__ bool segment(int32_t& pos, int32_t& end) {
+    if (!by_tile) {
+      if (started) return false;
+      started = true;
+      end = build_union();
+      pos = 0;
+      return true;
+    }
+    const int32_t* rown = arr(GroupLds<NT>::kRowN);
+    while (seg_t < T && seg_off >= rown[seg_t]) {
+      ++seg_t;
+      seg_off = 0;
+    }
+    if (seg_t >= T) return false;
+    end = build_window();
+    pos = 0;
+    seg_off += NT;
+    return true;
+  }
+};
+
+template <int KC>
+struct GroupSrc {
+  static constexpr bool kSparse = true;
+  static constexpr bool kGrouped = true;
+  GeoTable G;
+  const int32_t* row_ptr;
+  const int32_t* col_idx;
+  int32_t k, G_k;
+  int32_t gh, gw, lgT;   // group of gh x gw tiles, T = gh * gw = 1 << lgT
+  int32_t ngc, n_groups;  // groups per group row, groups per (b, h)
+  uint32_t wave_tile, wave_slab;  // 4 bits per wave: the wave's tile in the group and its 32-query slab
+  int32_t max_chunks_per_block;
+
+  template <int NT>
+  static constexpr int table_bytes() { return TableLds<NT>::kBytes + GroupLds<NT>::kBytes; }
+  __device__ __forceinline__ int tile_of(int wave) const { return (int)((wave_tile >> (4 * wave)) & 15u); }
+
+  // Tile t of the group of item; false when it lies outside the scale.
+  __device__ __forceinline__ bool group_tile(int32_t item, int t, int32_t& bh, int32_t& a, int32_t& c) const {
+    bh = item / n_groups;
+    const int32_t gi = item - bh * n_groups;
+    const int32_t A = gi / ngc, Cg = gi - A * ngc;
+    a = A * gh + t / gw;
+    c = Cg * gw + t % gw;
+    return a < G.Th[k - 1] && c < G.Tw[k - 1];
+  }
+  __device__ __forceinline__ QuerySet queries(int32_t item, int wave) const {
+    QuerySet s;
+    int32_t a, c;
+    const bool ok = group_tile(item, tile_of(wave), s.bh, a, c);
+    const Tile t = tile_at(G, k, ok ? a : 0, ok ? c : 0);
+    s.qbase = t.base - G.C[k - 1];
+    s.qnc = t.nc;
+    s.qstride = t.stride;
+    s.q0 = (int32_t)((wave_slab >> (4 * wave)) & 15u) * kQPerWave;
+    s.q1 = ok ? t.nr * t.nc : 0;
+    return s;
+  }
+  template <int NT>
+  __device__ __forceinline__ TableCursor<KC, NT, GroupBlocks<NT>> table_cursor(int32_t item, char* lds) const {
+    using L = GroupLds<NT>;
+    char* glds = lds + TableLds<NT>::kBytes;
+    const int T = 1 << lgT;
+    const int tid = threadIdx.x;
+    if (tid < T) {
+      int32_t bh, a, c;
+      int32_t p = 0, n = 0;
+      if (group_tile(item, tid, bh, a, c)) {
+        const int32_t r = bh * G_k + a * G.Tw[k - 1] + c;
+        p = row_ptr[r];
+        n = row_ptr[r + 1] - p;
+      }
+      reinterpret_cast<int32_t*>(glds + L::kRowP)[tid] = p;
+      reinterpret_cast<int32_t*>(glds + L::kRowN)[tid] = n;
+    }
+    __syncthreads();
+    const int32_t RC = NT >> lgT;
+    bool long_row = false;
+    for (int t = 0; t < T; ++t) long_row |= reinterpret_cast<const int32_t*>(glds + L::kRowN)[t] > RC;
+    TableCursor<KC, NT, GroupBlocks<NT>> cur;
+    cur.G = &G;
+    cur.blocks.col = col_idx;
+    cur.blocks.nb = G.NB[k];
+    cur.blocks.T = T;
+    cur.blocks.lgT = lgT;
+    cur.blocks.by_tile = long_row;
+    cur.blocks.started = false;
+    cur.blocks.seg_t = 0;
+    cur.blocks.seg_off = 0;
+    cur.blocks.lds = glds;
+    cur.nb = G.NB[k];
+    const int32_t g = kTableCap / (max_chunks_per_block > 0 ? max_chunks_per_block : 1);
+    cur.group = g < NT ? (g > 0 ? g : 1) : NT;
+    cur.pos = 0;
+    cur.end = 0;
+    cur.tn = 0;
+    cur.ti = 0;
+    cur.lds = lds;
+    return cur;
   }
 };
 
@@ -338,6 +627,23 @@ __device__ __forceinline__ int32_t swizzled_item(int32_t wg, int32_t n_wg, int32
   // range of items so neighbouring query tiles share that XCD's L2.
   const int32_t per = n_wg >> 3;  // n_wg is a multiple of 8 when swizzling
   return (wg & 7) * per + (wg >> 3);
+}
+
+// LDS pipeline stages as separate arrays: alias analysis then sees that the
+// direct HBM -> LDS copies into one stage cannot touch the stage being read,
+// and the compiler does not wait for those copies before every LDS read.
+#define SV_STAGE_ARRAYS(NSX, BYTES)                                              \
+  __shared__ __attribute__((aligned(16))) char sv_stage0[BYTES];                 \
+  __shared__ __attribute__((aligned(16))) char sv_stage1[BYTES];                 \
+  __shared__ __attribute__((aligned(16))) char sv_stage2[(NSX) > 2 ? (BYTES) : 16]; \
+  __shared__ __attribute__((aligned(16))) char sv_stage3[(NSX) > 3 ? (BYTES) : 16];
+
+template <int S>
+__device__ __forceinline__ char* stage_ptr(char* s0, char* s1, char* s2, char* s3) {
+  if constexpr (S == 0) return s0;
+  else if constexpr (S == 1) return s1;
+  else if constexpr (S == 2) return s2;
+  else return s3;
 }
 
 // ---------------------------------------------------------------- bf16 kernel
@@ -352,9 +658,10 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
   static_assert(KC % 32 == 0 && (KC * U) % NT == 0, "chunk must split evenly over the workgroup");
   static_assert(NS >= 2 && NS <= 4, "pipeline depth");
   static_assert(2 * kLoads * (NS - 2) < 64, "vmcnt range");
-  __shared__ __attribute__((aligned(16))) char smem[NS * kStage];
-  // chunk table of the sparse path (unused by the dense path)
-  constexpr int kTblBytes = Src::kSparse ? kTableCap * 8 + NT * 16 + (NT + 1) * 4 : 16;
+  SV_STAGE_ARRAYS(NS, kStage)
+#define SV_STAGE(S) stage_ptr<S>(sv_stage0, sv_stage1, sv_stage2, sv_stage3)
+  // chunk table of the sparse paths (unused by the dense path)
+  constexpr int kTblBytes = Src::template table_bytes<NT>();
   __shared__ __attribute__((aligned(16))) char tsmem[kTblBytes];
 
   const int32_t item = swizzled_item(blockIdx.x, gridDim.x, io.swizzle);
@@ -364,14 +671,15 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
   const int lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, half = lane >> 5;
 
-  const QuerySet qs = src.queries(item);
+  const QuerySet qs = src.queries(item, wave);
+  const int my_tile = src.tile_of(wave);  // bit of this wave's query tile in chunk masks
   const bf16_bits* qplane = static_cast<const bf16_bits*>(io.q) + (int64_t)qs.bh * io.q_bh_stride;
   const bf16_bits* kplane = static_cast<const bf16_bits*>(io.k) + (int64_t)qs.bh * io.kv_bh_stride;
   const bf16_bits* vplane = static_cast<const bf16_bits*>(io.v) + (int64_t)qs.bh * io.kv_bh_stride;
 
-  const int32_t qslot = qs.q0 + wave * kQPerWave + l32;
+  const int32_t qslot = qs.q0 + l32;
   const bool qvalid = qslot < qs.q1;
-  const int32_t qi = qvalid ? qslot : qs.q0;
+  const int32_t qi = qvalid ? qslot : 0;
   const int32_t qrow = qs.qbase + (qi / qs.qnc) * qs.qstride + (qi % qs.qnc);
   QFragBF16<D> qf;
   qf.load(qplane + (int64_t)qrow * D, half);
@@ -421,7 +729,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
   const char* vbytes = reinterpret_cast<const char*>(vplane);
   auto issue = [&](const Chunk& c, auto stage_c) {
     constexpr int S = decltype(stage_c)::value;
-    char* kb = smem + S * kStage;
+    char* kb = SV_STAGE(S);
 #pragma unroll
     for (int j = 0; j < kLoads; ++j) {
       const int first = (j * NW + wave_s) * 64;
@@ -434,9 +742,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
 
   auto cur = [&]() {
     if constexpr (Src::kSparse) {
-      return src.template table_cursor<NT>(item, reinterpret_cast<uint2*>(tsmem),
-                                           reinterpret_cast<int4*>(tsmem + kTableCap * 8),
-                                           reinterpret_cast<int32_t*>(tsmem + kTableCap * 8 + NT * 16));
+      return src.template table_cursor<NT>(item, tsmem);
     } else {
       return src.cursor(item);
     }
@@ -479,8 +785,10 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
     const bool have_n = ahead == NS - 2 && cur.next(cn);
     if (have_n) issue(cn, std::integral_constant<int, (S + NS - 1) % NS>{});
 
-    const char* kst = smem + S * kStage;
-
+    const char* kst = SV_STAGE(S);
+    // waves of a grouped launch skip chunks their query tile does not list
+    const bool active = !Src::kGrouped || ((c.mask >> my_tile) & 1u);
+    if (active) {
     // ---- S^T = K Q^T
     f32x16 st[KC / 32];
 #pragma unroll
@@ -548,6 +856,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
         acc[dt] = mfma_bf16(as_bf16x8(av), pf, acc[dt]);
       }
     }
+    }  // active
 
     // ---- advance the ring
 #pragma unroll
@@ -605,13 +914,13 @@ __global__ __launch_bounds__(NW * 64) void attn_f32_kernel(AttnIO io, Src src) {
   const int lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, half = lane >> 5;
 
-  const QuerySet qs = src.queries(item);
+  const QuerySet qs = src.queries(item, wave);
   const float* qplane = static_cast<const float*>(io.q) + (int64_t)qs.bh * io.q_bh_stride;
   const float* kplane = static_cast<const float*>(io.k) + (int64_t)qs.bh * io.kv_bh_stride;
   const float* vplane = static_cast<const float*>(io.v) + (int64_t)qs.bh * io.kv_bh_stride;
-  const int32_t qslot = qs.q0 + wave * kQPerWave + l32;
+  const int32_t qslot = qs.q0 + l32;
   const bool qvalid = qslot < qs.q1;
-  const int32_t qi = qvalid ? qslot : qs.q0;
+  const int32_t qi = qvalid ? qslot : 0;
   const int32_t qrow = qs.qbase + (qi / qs.qnc) * qs.qstride + (qi % qs.qnc);
   QFragF32<D> qf;
   qf.load(qplane + (int64_t)qrow * D, half);
@@ -843,11 +1152,164 @@ hipError_t launch_dense_attn(const DenseAttnArgs& a, hipStream_t stream) {
   return dispatch<DenseSrc>(a.bf16, a.d, nw, kc, ns, io, make, stream);
 }
 
+namespace {
+
+// Largest chunk count of any block of scales 1..k (full and edge tiles) at kc keys per chunk.
+int32_t max_chunks_per_block(const GeoTable& G, int k, int kc) {
+  int32_t maxc = 1;
+  for (int l = 1; l <= k; ++l) {
+    const int32_t eh = G.eh[l - 1], ew = G.ew[l - 1];
+    const int32_t rh[2] = {eh, G.h[l - 1] - (G.Th[l - 1] - 1) * eh};
+    const int32_t rw[2] = {ew, G.w[l - 1] - (G.Tw[l - 1] - 1) * ew};
+    for (int i = 0; i < 2; ++i)
+      for (int j = 0; j < 2; ++j) {
+        const int32_t nr = rh[i], nc = rw[j];
+        int32_t c;
+        if (nr == 1 || nc == G.w[l - 1]) c = (nr * nc + kc - 1) / kc;
+        else if (nc <= kc) c = (nr + kc / nc - 1) / (kc / nc);
+        else c = nr * ((nc + kc - 1) / kc);
+        maxc = c > maxc ? c : maxc;
+      }
+  }
+  return maxc;
+}
+
+// bf16 grouped launch shapes (d, waves, keys per chunk, pipeline stages).
+#define SV_GROUP_SHAPES(X)                                                                        \
+  X(128, 8, 64, 2) X(128, 8, 64, 3) X(128, 8, 64, 4) X(128, 8, 32, 2) X(128, 8, 32, 4) X(128, 4, 64, 2) \
+  X(128, 4, 64, 3) X(128, 4, 32, 2) X(64, 8, 64, 2) X(64, 8, 64, 3) X(64, 4, 64, 2)
+
+bool group_shape_exists(int d, int nw, int kc, int ns) {
+#define SV_HAS(DD, NN, KK, SS) \
+  if (d == DD && nw == NN && kc == KK && ns == SS) return true;
+  SV_GROUP_SHAPES(SV_HAS)
+#undef SV_HAS
+  return false;
+}
+
+// Waves to (tile, slab): tiles in order for the first four waves, then in
+// reverse tile order, so that when waves are dealt to the four SIMDs in turn a
+// SIMD holds waves of tiles far apart in the group and a chunk listed by only
+// some of the tiles still keeps several SIMDs busy.
+void wave_map(int nw, int T, int wpt, uint32_t* wave_tile, uint32_t* wave_slab) {
+  int tile[8], slab[8], n = 0;
+  for (int t = 0; t < T; ++t)
+    for (int s = 0; s < wpt; ++s) {
+      tile[n] = t;
+      slab[n] = s;
+      ++n;
+    }
+  int order[8];
+  for (int w = 0; w < nw; ++w) order[w] = w;
+  if (nw > 4) {
+    // waves 4.. take the remaining pairs by descending tile, ascending slab
+    int m = 4;
+    for (int t = T - 1; t >= 0; --t)
+      for (int p = 4; p < nw; ++p)
+        if (tile[p] == t) order[m++] = p;
+  }
+  *wave_tile = 0;
+  *wave_slab = 0;
+  for (int w = 0; w < nw; ++w) {
+    *wave_tile |= (uint32_t)tile[order[w]] << (4 * w);
+    *wave_slab |= (uint32_t)slab[order[w]] << (4 * w);
+  }
+}
+
+hipError_t launch_grouped(const SparseAttnArgs& a, int nw, int wpt, int kc, int ns, hipStream_t stream) {
+  const GeoTable& G = *a.G;
+  const int k = a.k;
+  const int T = nw / wpt;
+  int gh = 1, gw = 2, lgT = 1;
+  if (T == 4) {
+    gh = 2;
+    gw = 2;
+    lgT = 2;
+  } else if (T == 8) {
+    gh = 2;
+    gw = 4;
+    lgT = 3;
+  }
+  const int32_t ngr = (G.Th[k - 1] + gh - 1) / gh, ngc = (G.Tw[k - 1] + gw - 1) / gw;
+  AttnIO io;
+  io.q = a.q;
+  io.k = a.k_cache;
+  io.v = a.v_cache;
+  io.o = a.o;
+  io.lse = a.lse;
+  io.q_bh_stride = a.q_bh_stride;
+  io.kv_bh_stride = a.kv_bh_stride;
+  io.o_rows = G.h[k - 1] * G.w[k - 1];
+  io.n_items = a.BH * ngr * ngc;
+  io.swizzle = a.swizzle;
+  io.scale_log2 = a.softmax_scale * kLog2e;
+  GroupSrc<64> proto;
+  proto.G = G;
+  proto.row_ptr = a.row_ptr;
+  proto.col_idx = a.col_idx;
+  proto.k = k;
+  proto.G_k = tiles_of(G, k);
+  proto.gh = gh;
+  proto.gw = gw;
+  proto.lgT = lgT;
+  proto.ngc = ngc;
+  proto.n_groups = ngr * ngc;
+  wave_map(nw, T, wpt, &proto.wave_tile, &proto.wave_slab);
+  proto.max_chunks_per_block = max_chunks_per_block(G, k, kc);
+  auto as = [&](auto tag) {
+    decltype(tag) s;
+    s.G = proto.G;
+    s.row_ptr = proto.row_ptr;
+    s.col_idx = proto.col_idx;
+    s.k = proto.k;
+    s.G_k = proto.G_k;
+    s.gh = proto.gh;
+    s.gw = proto.gw;
+    s.lgT = proto.lgT;
+    s.ngc = proto.ngc;
+    s.n_groups = proto.n_groups;
+    s.wave_tile = proto.wave_tile;
+    s.wave_slab = proto.wave_slab;
+    s.max_chunks_per_block = proto.max_chunks_per_block;
+    return s;
+  };
+#define SV_GROUP(DD, NN, KK, SS) \
+  if (a.d == DD && nw == NN && kc == KK && ns == SS) return launch_bf16<DD, NN, KK, SS>(io, as(GroupSrc<KK>{}), stream);
+  SV_GROUP_SHAPES(SV_GROUP)
+#undef SV_GROUP
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
 hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream) {
   const GeoTable& G = *a.G;
   const int k = a.k;
   const int32_t tile_q = G.eh[k - 1] * G.ew[k - 1];
-  const int nw = a.waves > 0 ? a.waves : waves_for(tile_q);
+  const int wpt = waves_for(tile_q);
+  // grouped path: several query tiles per workgroup share each staged chunk.
+  // Automatic choice: pairs of 64-query tiles (or quads of 32-query tiles) in
+  // 4-wave workgroups, when that still gives every CU at least four workgroups;
+  // with fewer, the last round of workgroups runs the chip part-empty and one
+  // tile per workgroup is faster.
+  int gwv = a.group_waves;
+  if (gwv < 0) {
+    gwv = 0;
+    if (wpt <= 2) {
+      const int32_t gh = wpt == 2 ? 1 : 2, gw = 2;  // 1 x 2 or 2 x 2 tiles
+      const int64_t groups = (int64_t)a.BH * ((G.Th[k - 1] + gh - 1) / gh) * ((G.Tw[k - 1] + gw - 1) / gw);
+      if (groups >= 4 * (int64_t)a.num_cu) gwv = 4;
+    }
+  }
+  if (a.bf16 && a.waves <= 0 && gwv > wpt) {
+    int kc = a.group_chunk, ns = a.group_stages;
+    if (!group_shape_exists(a.d, gwv, kc, ns)) {
+      kc = 64;
+      ns = 2;
+    }
+    if (group_shape_exists(a.d, gwv, kc, ns)) return launch_grouped(a, gwv, wpt, kc, ns, stream);
+  }
+  const int nw = a.waves > 0 ? a.waves : wpt;
   int kc = 64, ns = 2;
   if (a.bf16) shape_for(a.d, nw, a.chunk, a.stages, &kc, &ns);
   const int32_t qpw = nw * kQPerWave;
@@ -865,22 +1327,7 @@ hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream) {
   io.n_items = a.BH * G_k * slabs;
   io.swizzle = a.swizzle;
   io.scale_log2 = a.softmax_scale * kLog2e;
-  // largest chunk count of any block of scales 1..k (full and edge tiles)
-  int32_t maxc = 1;
-  for (int l = 1; l <= k; ++l) {
-    const int32_t eh = G.eh[l - 1], ew = G.ew[l - 1];
-    const int32_t rh[2] = {eh, G.h[l - 1] - (G.Th[l - 1] - 1) * eh};
-    const int32_t rw[2] = {ew, G.w[l - 1] - (G.Tw[l - 1] - 1) * ew};
-    for (int i = 0; i < 2; ++i)
-      for (int j = 0; j < 2; ++j) {
-        const int32_t nr = rh[i], nc = rw[j];
-        int32_t c;
-        if (nr == 1 || nc == G.w[l - 1]) c = (nr * nc + kc - 1) / kc;
-        else if (nc <= kc) c = (nr + kc / nc - 1) / (kc / nc);
-        else c = nr * ((nc + kc - 1) / kc);
-        maxc = c > maxc ? c : maxc;
-      }
-  }
+  const int32_t maxc = max_chunks_per_block(G, k, kc);
   auto make = [&](auto proto) {
     auto s = proto;
     s.max_chunks_per_block = maxc;

@@ -29,8 +29,10 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
 // Keys of a chunk: slot s < count is token base + (s / nc) * stride + s % nc.
+// mask: query tiles of a workgroup's tile group that attend to the chunk (bit t for tile t).
 struct Chunk {
   int32_t base, nc, stride, count, magic;  // magic = ceil(65536 / nc): s / nc == (s * magic) >> 16 for s < 64
+  uint32_t mask;
 };
 
 __device__ __forceinline__ int32_t chunk_token(const Chunk& c, int32_t s) {
@@ -55,6 +57,7 @@ __device__ __forceinline__ Chunk make_chunk(int32_t base, int32_t nc, int32_t st
   c.stride = stride;
   c.count = count;
   c.magic = div_magic(nc);
+  c.mask = ~0u;
   return c;
 }
 
@@ -208,6 +211,38 @@ __device__ __forceinline__ void dma16(const void* g, char* lds) {
 // p points into __shared__ memory.
 __device__ __forceinline__ i16x4 lds_read_tr(const char* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(const_cast<char*>(p)));
+}
+
+// Inclusive prefix sum over the 64 lanes of a wave.
+__device__ __forceinline__ int32_t wave_incl_scan(int32_t x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int32_t y = __shfl_up(x, off, 64);
+    x += lane >= off ? y : 0;
+  }
+  return x;
+}
+
+// Exclusive prefix sum of x over the NT threads of the workgroup; total receives
+// the sum. wt: NT / 64 ints of LDS. Holds barriers: every thread must call it.
+template <int NT>
+__device__ __forceinline__ int32_t block_excl_scan(int32_t x, int32_t* wt, int32_t& total) {
+  constexpr int NW = NT / 64;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int32_t inc = wave_incl_scan(x);
+  if (lane == 63) wt[wave] = inc;
+  __syncthreads();
+  int32_t before = 0, all = 0;
+#pragma unroll
+  for (int w = 0; w < NW; ++w) {
+    const int32_t t = wt[w];
+    before += w < wave ? t : 0;
+    all += t;
+  }
+  __syncthreads();
+  total = all;
+  return before + inc - x;
 }
 
 // s_waitcnt immediate for "vmcnt <= n" (gfx9 encoding; expcnt and lgkmcnt left at max).

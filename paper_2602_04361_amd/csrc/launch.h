@@ -36,6 +36,10 @@ struct SparseAttnArgs {
   int chunk;    // keys per chunk (32 or 64)
   int stages;   // LDS pipeline depth
   int swizzle;
+  int group_waves;  // grouped path: waves per workgroup (4 or 8), 0 = one tile per workgroup, < 0 = auto
+  int group_chunk;  // grouped path: keys per chunk (32 or 64)
+  int group_stages; // grouped path: LDS pipeline depth
+  int num_cu;       // compute units of the device (automatic launch choices)
 };
 
 struct ScoreArgs {

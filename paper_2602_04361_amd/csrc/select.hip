@@ -152,7 +152,10 @@ __global__ __launch_bounds__(WPT * TPW * 64) void pooled_scores_kernel(ScoreIO i
   constexpr int KC = 64, NT = NW * 64, U = D / 8, kRow = D * 2, kTile = KC * kRow;
   constexpr int kLoads = KC * U / NT;
   static_assert((KC * U) % NT == 0, "chunk must split evenly over the workgroup");
-  __shared__ __attribute__((aligned(16))) char smem[2 * kTile];
+  // two K stages as separate arrays, so the compiler can tell that copies into
+  // one stage never touch the stage being read
+  __shared__ __attribute__((aligned(16))) char kstage0[kTile];
+  __shared__ __attribute__((aligned(16))) char kstage1[kTile];
   extern __shared__ float red[];  // [NW][per] per-wave block sums
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -199,7 +202,7 @@ __global__ __launch_bounds__(WPT * TPW * 64) void pooled_scores_kernel(ScoreIO i
       const int first = (j * NW + wave_s) * 64;
       const int r = ld_row[j];
       const uint32_t off = (uint32_t)(chunk_token(c, r < c.count ? r : 0) * D + 8 * ld_unit[j]) * 2u;
-      dma16(kbytes + off, smem + SG * kTile + first * 16);
+      dma16(kbytes + off, (SG == 0 ? kstage0 : kstage1) + first * 16);
     }
   };
 
@@ -225,7 +228,7 @@ __global__ __launch_bounds__(WPT * TPW * 64) void pooled_scores_kernel(ScoreIO i
     bool lastn = false;
     const bool have_n = walk.next(cn, bn, lastn);
     if (have_n) issue(cn, std::integral_constant<int, SG ^ 1>{});
-    const char* kst = smem + SG * kTile;
+    const char* kst = SG == 0 ? kstage0 : kstage1;
     f32x16 st[2];
     st[0] = zero16();
     st[1] = zero16();

@@ -1,0 +1,111 @@
+"""GPU parity of every launch form of the block-sparse kernel against the fp64
+oracle: one query tile per workgroup, and groups of 2, 4 or 8 neighbouring
+tiles per workgroup walking the union of their rows (each tile still attends
+to exactly its own blocks). The form is chosen through the library's launch
+knobs, read at every call.
+
+Rows are seeded random ascending block subsets with out-of-range ids mixed in
+(skipped by definition), empty rows, and rows longer than a group's merge
+capacity (those groups are served tile by tile).
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+from gpu_helpers import INF_SIDES, assert_close, make_case, note, oracle_geometry, scale_of, to_dev
+from paper_2602_04361_amd import sparvar as sv
+from test_gpu_parity import run_case
+
+pytestmark = pytest.mark.gpu
+
+FORMS = {
+    "per_tile": {"SPARVAR_SPARSE_GROUP_WAVES": "0"},
+    "group4": {"SPARVAR_SPARSE_GROUP_WAVES": "4"},
+    "group8": {"SPARVAR_SPARSE_GROUP_WAVES": "8"},
+    "group8_kc32": {"SPARVAR_SPARSE_GROUP_WAVES": "8", "SPARVAR_SPARSE_GROUP_CHUNK": "32"},
+}
+
+
+def random_rows(nb, n_rows, rng, long_every, long_len, short_len):
+    rows, clean = [], []
+    for g in range(n_rows):
+        if g % 11 == 5:
+            n = 0
+        elif long_every and g % long_every == 0:
+            n = min(long_len, nb)
+        else:
+            n = int(rng.integers(1, short_len + 1))
+        ids = sorted(rng.choice(nb, size=n, replace=False).tolist())
+        row = list(ids)
+        for _ in range(int(rng.integers(0, 3))):
+            row.insert(int(rng.integers(0, len(row) + 1)), int(rng.choice([-1, -5, nb, nb + 7])))
+        rows.append(row)
+        clean.append(ids)
+    return rows, clean
+
+
+def run_rows(monkeypatch, form, h, w, b, ns, k, B, H, d, seed, long_every, long_len, short_len):
+    for key, val in FORMS[form].items():
+        monkeypatch.setenv(key, val)
+    note(f"[grouped] form={form} h={h} w={w} b={b} k={k} B={B} H={H} d={d} seed={seed}")
+    q, kk, v = make_case(h, w, B, H, d, 8, ns, seed, "bf16")
+    og = oracle_geometry(h, w, b, ns)
+    g = sv.Geometry(h, w, b, ns)
+    Q, K, V = to_dev(q, "bf16"), to_dev(kk, "bf16"), to_dev(v, "bf16")
+    rng = np.random.default_rng(seed)
+    BH, G_k, nb = B * H, og.tiles(k), og.nb_le(k)
+    rows, clean = random_rows(nb, BH * G_k, rng, long_every, long_len, short_len)
+    ptr, col = O.rows_to_csr(rows)
+    rp = torch.tensor(ptr, dtype=torch.int32, device="cuda")
+    ci = torch.tensor(col, dtype=torch.int32, device="cuda")
+    o = torch.full((B, H, og.N(k), d), 3.0, dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty(B, H, og.N(k), device="cuda")
+    C0, C1 = og.C(k - 1), og.C(k)
+    sv.sparvar_block_sparse_attn_fwd(g, k, Q[:, :, C0:C1], K[:, :, :C1], V[:, :, :C1], o, rp, ci, lse=lse,
+                                     softmax_scale=scale_of(d))
+    torch.cuda.synchronize()
+    got = o.float().cpu().numpy().reshape(BH, -1, d)
+    gl = lse.cpu().numpy().reshape(BH, -1)
+    qf, kf, vf = q.reshape(BH, -1, d), kk.reshape(BH, -1, d), v.reshape(BH, -1, d)
+    for bh in range(BH):
+        per = clean[bh * G_k:(bh + 1) * G_k]
+        o_ref, l_ref = O.block_sparse_attention_gather(qf[bh, C0:C1], kf[bh, :C1], vf[bh, :C1], og, k, per,
+                                                       scale_of(d))
+        assert_close(got[bh], o_ref, "bf16", f"{form} O head {bh}")
+        fin = np.isfinite(l_ref)
+        assert (np.isneginf(gl[bh]) == ~fin).all(), f"{form} empty rows head {bh}"
+        assert np.abs(gl[bh][fin] - l_ref[fin]).max() <= 2e-4, f"{form} LSE head {bh}"
+    return got
+
+
+@pytest.mark.parametrize("form", list(FORMS))
+def test_forms_infinity_last_scale(monkeypatch, form):
+    # 8x8 tiles at 64x64 (2 waves a tile); every 9th row longer than 128 blocks
+    run_rows(monkeypatch, form, INF_SIDES, INF_SIDES, 8, 4, 13, 1, 2, 128, 21, 9, 140, 40)
+
+
+@pytest.mark.parametrize("form", ["per_tile", "group4", "group8"])
+def test_forms_small_tiles_partial_groups(monkeypatch, form):
+    # 4x4 tiles (16 queries, one wave a tile) on a 27x27 scale: edge tiles 3 wide
+    # and groups hanging over the scale's edge; rows of 70 blocks exceed the
+    # merge capacity of 64 entries per tile
+    h = [1, 2, 3, 5, 7, 10, 13, 20, 27]
+    run_rows(monkeypatch, form, h, h, 4, 2, 9, 1, 2, 64, 22, 7, 70, 20)
+
+
+@pytest.mark.parametrize("form", ["group4", "group8"])
+def test_forms_nonsquare_d64(monkeypatch, form):
+    h = [1, 2, 3, 5, 8, 11, 17]
+    w = [1, 3, 4, 7, 9, 14, 21]
+    run_rows(monkeypatch, form, h, w, 8, 2, 7, 2, 2, 64, 23, 0, 0, 12)
+
+
+@pytest.mark.parametrize("form", ["per_tile", "group4"])
+def test_forms_on_pipeline_rows(monkeypatch, form):
+    # The whole path (decision, mapping, attention at 40/48/64) with the rows the
+    # mapping step writes; the automatic form is covered by the parity suite.
+    for key, val in FORMS[form].items():
+        monkeypatch.setenv(key, val)
+    run_case(INF_SIDES, INF_SIDES, 8, 4, 10, [11, 12, 13], 1, 4, 128, 32, 8, 1, "bf16", seed=12,
+             tiles_per_step=16)
