@@ -2,7 +2,8 @@
 
 One step = one layer of the whole hot path on the Infinity 1024x1024 schedule
 (scales 1,2,4,6,8,12,16,20,24,32,40,48,64; B=2 CFG pair, H=16, d=128, bf16):
-  decision scale 32x32: dense attention + LSE, pooled block scores, top-8;
+  decision scale 32x32: dense attention + LSE, pooled block scores and top-8
+  (one fused call);
   for each sparse step 40x40, 48x48, 64x64: index mapping into CSR (the sink and
   local rows are generated inside the mapping call), block-sparse attention
   (8x8-token blocks, sinks = scales 1-4, 3x3 window).
@@ -10,8 +11,8 @@ Inputs are seeded synthetic tensors resident in HBM; four input sets rotate so
 no step finds its K/V in cache from the previous one.
 
 Prints one JSON line. `value` is the algorithmic TFLOP/s of the whole step
-(4 d * kept query-key pairs, plus the decision-scale dense and scoring
-FLOPs) over the measured step time.
+(4 d * attended query-key pairs: the dense decision scale plus the kept pairs
+of the three sparse steps) over the measured step time.
 """
 from __future__ import annotations
 
@@ -198,22 +199,16 @@ def main():
     info = path.info
     stream = torch.cuda.current_stream()
 
-    names = ["dense_S", "select", "map_11", "attn_11", "map_12", "attn_12", "map_13", "attn_13"]
+    names = ["decision", "map_11", "attn_11", "map_12", "attn_12", "map_13", "attn_13"]
 
     def one_step(i, ev=None):
         Q, K, V = sets[i % len(sets)]
         if ev is not None:
             ev[0].record(stream)
-        S = CFG["S"]
-        qS, kS, vS = path.q_slice(Q, S), path.kv_prefix(K, S), path.kv_prefix(V, S)
-        sv.sparvar_dense_attn_fwd(qS, kS, vS, path.o_S, path.lse_S, softmax_scale=path.scale)
+        path.decision(Q, K, V)
         if ev is not None:
             ev[1].record(stream)
-        sv.sparvar_select_blocks(g, S, qS, kS, path.lse_S, path.topk, path.topk_idx, scores_out=path.scores,
-                                 softmax_scale=path.scale)
-        if ev is not None:
-            ev[2].record(stream)
-        j = 3
+        j = 2
         for kk in CFG["steps"]:
             path.map_step(kk)
             if ev is not None:
@@ -236,8 +231,7 @@ def main():
         acct[kk] = sparse_accounting(rp.cpu().numpy(), ci.cpu().numpy(), info, kk, BH, d)
     iS = info[CFG["S"]]
     dense_S_flops = 4.0 * d * BH * iS["n_tokens"] * iS["n_tokens_le"]
-    score_flops = 2.0 * d * BH * iS["n_tokens"] * iS["n_tokens_le"]
-    step_flops = dense_S_flops + score_flops + sum(a[0] for a in acct.values())
+    step_flops = dense_S_flops + sum(a[0] for a in acct.values())
 
     # timed region
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(args.steps)]
@@ -280,12 +274,8 @@ def main():
 
     f13, b13, dens13, _ = acct[13]
     attn13_ms = per["attn_13"]
-    kernels = {
-        "dense_S": {"ms": per["dense_S"], "tflops": dense_S_flops / per["dense_S"] / 1e9},
-        "select": {"ms": per["select"], "tflops": score_flops / per["select"] / 1e9},
-    }
-    for n in ("dense_S", "select"):
-        kernels[n].update({"ms_" + q: v for q, v in spread[n].items()})
+    kernels = {"decision": {"ms": per["decision"], "tflops": dense_S_flops / per["decision"] / 1e9,
+                            **{"ms_" + q: v for q, v in spread["decision"].items()}}}
     for kk in CFG["steps"]:
         f, b_, dens, keys = acct[kk]
         side = info[kk]["h"]
@@ -332,7 +322,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) Q/K/V + 2-D sinusoidal position features + sink bias), 4 rotating sets",
-        "config": {"workload": "Infinity 1024x1024 schedule, one layer: dense+select at 32x32, "
+        "config": {"workload": "Infinity 1024x1024 schedule, one layer: dense attention + selection at 32x32, "
                                "block-sparse steps 40x40/48x48/64x64", "batch": B, "heads": H, "head_dim": d,
                    "block": "8x8 tokens", "topk": CFG["topk"], "window_radius": CFG["radius"],
                    "sink_scales": CFG["n_sink"], "kv_tokens_last_step": info[13]["n_tokens_le"]},

@@ -130,6 +130,29 @@ int sparvar_select_blocks(const sparvar_geometry_t* g, int32_t S, int32_t B, int
                           hipStream_t stream);
 
 /*
+ * The whole decision step at scale S in one call (Sec. 3.2): dense attention
+ * of the scale-S queries over the keys of scales 1..S (O_S, LSE_S), the pooled
+ * block scores and the per-tile top-k -- the results of sparvar_dense_attn_fwd
+ * followed by sparvar_select_blocks, but for bf16 in one fused launch that
+ * takes each block's probability mass from the attention pass itself (no
+ * second S = Q K^T pass). fp32 inputs, tiles wider than 32 tokens or candidate
+ * sets too large for the fused kernel's LDS run the two-call sequence instead.
+ *   q_S: [B,H,N_S,d] (plane stride q_bh_stride); k_leS, v_leS: [B,H,N_<=S,d]
+ *   (plane stride kv_bh_stride); o_S: [B,H,N_S,d] contiguous; lse_S: [B,H,N_S]
+ *   fp32; scores_out: fp32 [B,H,G_S,NB_<=S]; topk_idx: int32 [B,H,G_S,topk]
+ *   (ascending ids, -1 padding when topk > NB_<=S). All required.
+ *   Scores and ids follow sparvar_select_blocks' definitions; the scores are
+ *   computed in a different order, so equal-score ties may resolve
+ *   differently from the two-call path at the last bit.
+ * Requires 1 <= S <= num_scales, 1 <= topk <= 1024.
+ */
+int sparvar_decision_step(const sparvar_geometry_t* g, int32_t S, int32_t B, int32_t H, int32_t d,
+                          sparvar_dtype_t dtype, const void* q_S, int64_t q_bh_stride,
+                          const void* k_leS, const void* v_leS, int64_t kv_bh_stride, void* o_S,
+                          float* lse_S, float softmax_scale, float* scores_out, int32_t topk,
+                          int32_t* topk_idx, hipStream_t stream);
+
+/*
  * Sink + cross-scale local blocks of every query tile of scale k (block form
  * of the CSLA mask, Sec. 3.3, and the sink set of the appendix). Row g
  * (query tile (a,c) = (g / T_w(k), g % T_w(k))) lists ascending:

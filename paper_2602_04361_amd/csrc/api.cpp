@@ -241,6 +241,57 @@ int sparvar_select_blocks(const sparvar_geometry_t* g, int32_t S, int32_t B, int
   return hip_status(launch_topk(sel_in, (int32_t)rows, NB, topk, topk_idx, stream), "top-k launch");
 }
 
+int sparvar_decision_step(const sparvar_geometry_t* g, int32_t S, int32_t B, int32_t H, int32_t d,
+                          sparvar_dtype_t dtype, const void* q_S, int64_t q_bh_stride,
+                          const void* k_leS, const void* v_leS, int64_t kv_bh_stride, void* o_S,
+                          float* lse_S, float softmax_scale, float* scores_out, int32_t topk,
+                          int32_t* topk_idx, hipStream_t stream) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if (S < 1 || S > T.L) return fail(SPARVAR_ERR_INVALID, "decision scale %d outside [1, %d]", S, T.L);
+  if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
+  if ((st = check_dtype_d(dtype, d))) return st;
+  if (topk < 1 || topk > 1024) return fail(SPARVAR_ERR_INVALID, "topk %d outside [1, 1024]", topk);
+  if (!lse_S || !scores_out || !topk_idx) return fail(SPARVAR_ERR_INVALID, "lse_S, scores_out and topk_idx are required");
+  if (!(std::isfinite(softmax_scale))) return fail(SPARVAR_ERR_INVALID, "softmax_scale is not finite");
+  const int elem = dtype == SPARVAR_BF16 ? 2 : 4;
+  const int32_t NS = T.h[S - 1] * T.w[S - 1];
+  const int32_t NB = T.NB[S];
+  if ((st = check_plane(q_S, q_bh_stride, NS, d, elem, "q_S"))) return st;
+  if ((st = check_plane(k_leS, kv_bh_stride, T.C[S], d, elem, "k_leS"))) return st;
+  if ((st = check_plane(v_leS, kv_bh_stride, T.C[S], d, elem, "v_leS"))) return st;
+  if ((st = check_plane(o_S, (int64_t)NS * d, NS, d, elem, "o_S"))) return st;
+  const int64_t rows = (int64_t)B * H * tiles_of(T, S);
+  if ((int64_t)B * H * NS >= (int64_t(1) << 31) || rows * (NB > topk ? NB : topk) >= (int64_t(1) << 31))
+    return fail(SPARVAR_ERR_INVALID, "tensors too large");
+  if (dtype == SPARVAR_BF16 && decision_supported(T, S, d, NB, nullptr)) {
+    DecisionArgs a;
+    a.G = &T;
+    a.S = S;
+    a.BH = B * H;
+    a.d = d;
+    a.q = q_S;
+    a.k = k_leS;
+    a.v = v_leS;
+    a.o = o_S;
+    a.lse = lse_S;
+    a.q_bh_stride = q_bh_stride;
+    a.kv_bh_stride = kv_bh_stride;
+    a.softmax_scale = softmax_scale;
+    a.scores = scores_out;
+    a.topk = topk;
+    a.topk_idx = topk_idx;
+    a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
+    return hip_status(launch_decision(a, stream), "decision step launch");
+  }
+  if ((st = sparvar_dense_attn_fwd(B, H, NS, T.C[S], d, dtype, q_S, q_bh_stride, k_leS, v_leS, kv_bh_stride, o_S,
+                                   lse_S, softmax_scale, stream)))
+    return st;
+  return sparvar_select_blocks(g, S, B, H, d, dtype, q_S, q_bh_stride, k_leS, kv_bh_stride, lse_S, softmax_scale,
+                               nullptr, scores_out, topk, topk_idx, stream);
+}
+
 int64_t sparvar_local_blocks_capacity(const sparvar_geometry_t* g, int32_t k, int32_t radius,
                                       int32_t prev_dilation) {
   GeoTable T;

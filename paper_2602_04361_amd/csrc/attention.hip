@@ -621,13 +621,6 @@ struct GroupSrc {
   }
 };
 
-__device__ __forceinline__ int32_t swizzled_item(int32_t wg, int32_t n_wg, int32_t on) {
-  if (!on) return wg;
-  // Workgroups are dealt round-robin to the 8 XCDs; give each XCD a contiguous
-  // range of items so neighbouring query tiles share that XCD's L2.
-  const int32_t per = n_wg >> 3;  // n_wg is a multiple of 8 when swizzling
-  return (wg & 7) * per + (wg >> 3);
-}
 
 // LDS pipeline stages as separate arrays: alias analysis then sees that the
 // direct HBM -> LDS copies into one stage cannot touch the stage being read,

@@ -188,6 +188,61 @@ __device__ __forceinline__ int key_of(int kt, int r, int half) {
   return 32 * kt + 8 * (r >> 2) + 4 * half + (r & 3);
 }
 
+// Blocks [first, end) in id order, each cut into bands of whole tile rows of at
+// most KC keys (a block never shares a chunk with another block). Tiles must be
+// at most KC tokens wide.
+template <int KC>
+struct BlockWalker {
+  const GeoTable* G;
+  int32_t l, tu, tv, r0, v, nb;
+  Tile t;
+  // walk blocks [first, end)
+  __device__ __forceinline__ void start(const GeoTable* g, int32_t first, int32_t end) {
+    G = g;
+    nb = end;
+    v = first;
+    r0 = 0;
+    if (v < nb) {
+      l = block_scale(*G, v);
+      const int32_t t0 = v - G->NB[l - 1];
+      tu = (int32_t)div_by_magic((uint32_t)t0, G->mTw[l - 1]);
+      tv = t0 - tu * G->Tw[l - 1];
+      t = tile_at(*G, l, tu, tv);
+    }
+  }
+  // Next chunk; `blk` is its block id and `last` tells whether it ends that block.
+  __device__ __forceinline__ bool next(Chunk& c, int32_t& blk, bool& last) {
+    if (v >= nb) return false;
+    const int32_t rpc = KC / t.nc;  // t.nc <= block edge <= 64 = KC
+    const int32_t rows = (t.nr - r0 < rpc) ? t.nr - r0 : rpc;
+    c = make_chunk(t.base + r0 * t.stride, t.nc, t.stride, rows * t.nc);
+    blk = v;
+    r0 += rows;
+    last = r0 >= t.nr;
+    if (last) {
+      ++v;
+      r0 = 0;
+      if (++tv == G->Tw[l - 1]) {
+        tv = 0;
+        if (++tu == G->Th[l - 1]) {
+          tu = 0;
+          ++l;
+        }
+      }
+      if (v < nb) t = tile_at(*G, l, tu, tv);
+    }
+    return true;
+  }
+};
+
+__device__ __forceinline__ int32_t swizzled_item(int32_t wg, int32_t n_wg, int32_t on) {
+  if (!on) return wg;
+  // Workgroups are dealt round-robin to the 8 XCDs; give each XCD a contiguous
+  // range of items so neighbouring query tiles share that XCD's L2.
+  const int32_t per = n_wg >> 3;  // n_wg is a multiple of 8 when swizzling
+  return (wg & 7) * per + (wg >> 3);
+}
+
 // Uniform (wave-invariant) value hint.
 __device__ __forceinline__ int32_t uniform(int32_t x) { return __builtin_amdgcn_readfirstlane(x); }
 

@@ -54,7 +54,24 @@ struct ScoreArgs {
 };
 
 hipError_t launch_dense_attn(const DenseAttnArgs& a, hipStream_t stream);
+struct DecisionArgs {
+  const GeoTable* G;
+  int32_t S, BH, d;
+  const void *q, *k, *v;
+  void* o;
+  float* lse;
+  int64_t q_bh_stride, kv_bh_stride;
+  float softmax_scale;
+  float* scores;
+  int32_t topk;
+  int32_t* topk_idx;
+  int swizzle;
+};
+
 hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream);
+// fused dense attention + LSE + pooled scores + top-k at the decision scale (bf16)
+bool decision_supported(const GeoTable& G, int S, int d, int32_t NB, size_t* lds_bytes);
+hipError_t launch_decision(const DecisionArgs& a, hipStream_t stream);
 hipError_t launch_pooled_scores(const ScoreArgs& a, hipStream_t stream);
 hipError_t launch_topk(const float* scores, int32_t rows, int32_t nb, int32_t topk, int32_t* out,
                        hipStream_t stream);

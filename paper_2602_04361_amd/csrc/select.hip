@@ -92,51 +92,6 @@ __global__ __launch_bounds__(NW * 64) void pooled_scores_f32_kernel(ScoreIO io) 
   }
 }
 
-// Blocks 0..NB-1 of scales 1..S in id order, each cut into bands of whole tile
-// rows of at most KC keys (a block never shares a chunk with another block).
-template <int KC>
-struct BlockWalker {
-  const GeoTable* G;
-  int32_t l, tu, tv, r0, v, nb;
-  Tile t;
-  // walk blocks [first, end)
-  __device__ __forceinline__ void start(const GeoTable* g, int32_t first, int32_t end) {
-    G = g;
-    nb = end;
-    v = first;
-    r0 = 0;
-    if (v < nb) {
-      l = block_scale(*G, v);
-      const int32_t t0 = v - G->NB[l - 1];
-      tu = (int32_t)div_by_magic((uint32_t)t0, G->mTw[l - 1]);
-      tv = t0 - tu * G->Tw[l - 1];
-      t = tile_at(*G, l, tu, tv);
-    }
-  }
-  // Next chunk; `blk` is its block id and `last` tells whether it ends that block.
-  __device__ __forceinline__ bool next(Chunk& c, int32_t& blk, bool& last) {
-    if (v >= nb) return false;
-    const int32_t rpc = KC / t.nc;  // t.nc <= block edge <= 64 = KC
-    const int32_t rows = (t.nr - r0 < rpc) ? t.nr - r0 : rpc;
-    c = make_chunk(t.base + r0 * t.stride, t.nc, t.stride, rows * t.nc);
-    blk = v;
-    r0 += rows;
-    last = r0 >= t.nr;
-    if (last) {
-      ++v;
-      r0 = 0;
-      if (++tv == G->Tw[l - 1]) {
-        tv = 0;
-        if (++tu == G->Th[l - 1]) {
-          tu = 0;
-          ++l;
-        }
-      }
-      if (v < nb) t = tile_at(*G, l, tu, tv);
-    }
-    return true;
-  }
-};
 
 // bf16 scoring: one workgroup per (b, h, group of TPW query tiles of scale S),
 // WPT waves per tile. Every query of a head scores against all keys of scales

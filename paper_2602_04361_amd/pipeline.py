@@ -2,8 +2,10 @@
 
 SparsePath owns the device buffers (allocated with torch) and issues, on the
 current stream:
-  decision(): dense attention with LSE at the decision scale S, then pooled
-              block scores and per-query-tile top-k (sparvar_select_blocks);
+  decision(): dense attention with LSE at the decision scale S, pooled block
+              scores and per-query-tile top-k in one sparvar_decision_step
+              call (or, with fused=False, sparvar_dense_attn_fwd followed by
+              sparvar_select_blocks);
   step(k):    sparvar_map_index (mapped + local blocks -> CSR + schedule), then
               sparvar_block_sparse_attn_fwd at scale k.
 Local rows are geometry-only and built once per step by build_local().
@@ -20,7 +22,8 @@ from . import sparvar as sv
 
 class SparsePath:
     def __init__(self, geom: sv.Geometry, S, steps, B, H, d, topk, radius, prev_dilation=0,
-                 dtype=torch.bfloat16, device="cuda", use_schedule=False, softmax_scale=None, local_lists=False):
+                 dtype=torch.bfloat16, device="cuda", use_schedule=False, softmax_scale=None, local_lists=False,
+                 fused_decision=True):
         self.g = geom
         self.S, self.steps = int(S), [int(k) for k in steps]
         self.B, self.H, self.d = B, H, d
@@ -29,6 +32,7 @@ class SparsePath:
         # local_lists: build the sink + local rows once with sparvar_local_blocks and
         # pass them to the mapping; otherwise the mapping generates them itself.
         self.local_lists = local_lists
+        self.fused_decision = fused_decision
         self.scale = float(torch.tensor(1.0 / math.sqrt(d), dtype=torch.float32)) if softmax_scale is None \
             else float(softmax_scale)
         info = {l: geom.scale_info(l) for l in range(1, len(geom.h) + 1)}
@@ -68,6 +72,10 @@ class SparsePath:
     def decision(self, Q_all, K_all, V_all):
         S = self.S
         q, kk, vv = self.q_slice(Q_all, S), self.kv_prefix(K_all, S), self.kv_prefix(V_all, S)
+        if self.fused_decision:
+            sv.sparvar_decision_step(self.g, S, q, kk, vv, self.o_S, self.lse_S, self.scores, self.topk,
+                                     self.topk_idx, softmax_scale=self.scale)
+            return
         sv.sparvar_dense_attn_fwd(q, kk, vv, self.o_S, self.lse_S, softmax_scale=self.scale)
         sv.sparvar_select_blocks(self.g, S, q, kk, self.lse_S, self.topk, self.topk_idx, scores_out=self.scores,
                                  softmax_scale=self.scale)

@@ -22,6 +22,7 @@ EXPORTS = [
     "sparvar_scale_info",
     "sparvar_dense_attn_fwd",
     "sparvar_select_blocks",
+    "sparvar_decision_step",
     "sparvar_local_blocks_capacity",
     "sparvar_local_blocks",
     "sparvar_map_index_capacity",
@@ -73,6 +74,8 @@ def load_library(path: str = LIB_PATH):
                                                   vp, f32, vp]),
         "sparvar_select_blocks": (ctypes.c_int, [G, i32, i32, i32, i32, ctypes.c_int, vp, i64, vp, i64, vp, f32, vp,
                                                  vp, i32, vp, vp]),
+        "sparvar_decision_step": (ctypes.c_int, [G, i32, i32, i32, i32, ctypes.c_int, vp, i64, vp, vp, i64, vp, vp,
+                                                 f32, vp, i32, vp, vp]),
         "sparvar_local_blocks_capacity": (i64, [G, i32, i32, i32]),
         "sparvar_local_blocks": (ctypes.c_int, [G, i32, i32, i32, vp, vp, i64, vp]),
         "sparvar_map_index_capacity": (i64, [G, i32, i32, i32, i32, i32, i32, i32]),
@@ -190,6 +193,20 @@ def sparvar_select_blocks(geom, S, q_S, k_leS, lse_S, topk, topk_idx, scores_out
     _check(lib.sparvar_select_blocks(geom.ref, S, B, H, d, dt, _ptr(q_S), qs, _ptr(k_leS), ks, _ptr(lse_S),
                                      _scale(softmax_scale, d), _ptr(scores_in), _ptr(scores_out), topk,
                                      _ptr(topk_idx), _stream(stream)))
+    return topk_idx
+
+
+def sparvar_decision_step(geom, S, q_S, k_leS, v_leS, o_S, lse_S, scores_out, topk, topk_idx, softmax_scale=None,
+                          stream=None):
+    """Dense attention + LSE, pooled scores and top-k at the decision scale; see sparvar.h."""
+    lib = load_library()
+    B, H, _, d = q_S.shape
+    if _plane_stride(v_leS, "v_leS") != _plane_stride(k_leS, "k_leS"):
+        raise SparvarError(ERR_INVALID, "k_leS and v_leS must share one plane stride")
+    _check(lib.sparvar_decision_step(geom.ref, S, B, H, d, _dtype_code(q_S), _ptr(q_S), _plane_stride(q_S, "q_S"),
+                                     _ptr(k_leS), _ptr(v_leS), _plane_stride(k_leS, "k_leS"), _ptr(o_S), _ptr(lse_S),
+                                     _scale(softmax_scale, d), _ptr(scores_out), topk, _ptr(topk_idx),
+                                     _stream(stream)))
     return topk_idx
 
 

@@ -125,3 +125,25 @@ def test_attention_validation_before_launch():
     assert lib.sparvar_map_index(g.ref, 10, 13, 1, 1, 8, fake, fake, fake, 1, 0, fake, fake, 10, None,
                                  None) == sv.ERR_CAPACITY
     assert b"capacity" in lib.sparvar_last_error()
+
+
+def test_decision_step_validation_before_launch():
+    lib = sv.load_library()
+    vp = ctypes.c_void_p
+    fake = vp(1 << 20)
+    g = sv.Geometry(INF, INF, 8, 4)
+    args = lambda **kw: dict(dict(S=10, B=1, H=1, d=128, dt=sv.BF16, q=fake, qs=1024 * 128, k=fake, v=fake,
+                                  kvs=2521 * 128, o=fake, lse=fake, scale=0.1, scores=fake, topk=8, idx=fake), **kw)
+
+    def call(a):
+        return lib.sparvar_decision_step(g.ref, a["S"], a["B"], a["H"], a["d"], a["dt"], a["q"], a["qs"], a["k"],
+                                         a["v"], a["kvs"], a["o"], a["lse"], a["scale"], a["scores"], a["topk"],
+                                         a["idx"], None)
+    assert call(args(S=14)) == sv.ERR_INVALID          # scale out of range
+    assert call(args(d=96)) == sv.ERR_UNSUPPORTED      # head dim
+    assert call(args(topk=0)) == sv.ERR_INVALID        # top-k range
+    assert call(args(lse=None)) == sv.ERR_INVALID      # LSE, scores and ids are required
+    assert call(args(scores=None)) == sv.ERR_INVALID
+    assert call(args(v=None)) == sv.ERR_INVALID
+    assert call(args(kvs=100)) == sv.ERR_INVALID       # plane stride shorter than the plane
+    assert call(args(scale=float("inf"))) == sv.ERR_INVALID
