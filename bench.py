@@ -47,6 +47,9 @@ def parse():
     ap.add_argument("--sets", type=int, default=N_SETS)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="finish with three plain device copies of 256 MiB (reference for HBM byte counters)")
+    ap.add_argument("--sweep", action="store_true",
+                    help="instead of the step line: one JSON line per setting of the wider-head, 2048x2048 and "
+                         "sparsity-sweep workloads (per-layer times, TFLOP/s, density, speedup)")
     return ap.parse_args()
 
 
@@ -122,7 +125,7 @@ def cpu_baseline(q, k, v, target_s):
         O.dense_attention(qS, kS, vS, sc)
         scores = O.pooled_scores(qS, kS, sc, g, S)
         tk = np.array([[O.topk_blocks(r, CFG["topk"]) for r in scores]])
-        flops_done += 4.0 * d * g.N(S) * g.C(S) + 2.0 * d * g.N(S) * g.C(S)
+        flops_done += 4.0 * d * g.N(S) * g.C(S)
         for kk in CFG["steps"]:
             rows = O.build_rows(g, S, kk, tk, local[kk])[0]
             O.block_sparse_attention_gather(qf[bh, g.C(kk - 1):g.C(kk)], kf[bh, :g.C(kk)], vf[bh, :g.C(kk)], g, kk,
@@ -167,6 +170,105 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
+# ---------------------------------------------------------------- sweep of the other workloads
+SWEEP = ([dict(name="heads32", sides=SIDES, B=2, H=32, b=8, S=10, steps=[11, 12, 13], topk=8, radius=1, sets=4),
+          dict(name="schedule2048", sides=SIDES + [80, 96, 128], B=1, H=16, b=8, S=13, steps=[14, 15, 16], topk=16,
+               radius=1, sets=2)] +
+         [dict(name=f"last_step_b{b}_r{r}_top{t}", sides=SIDES, B=2, H=16, b=b, S=10, steps=[13], topk=t, radius=r,
+               sets=4) for b in (8, 16) for r in (1, 2) for t in (4, 8, 16, 32)])
+
+
+def sweep(args, dev):
+    import torch
+
+    from paper_2602_04361_amd import sparvar as sv
+    from paper_2602_04361_amd.pipeline import SparsePath
+    from paper_2602_04361_amd.synth import make_qkv
+
+    d, nf, ns = CFG["d"], CFG["n_freq"], CFG["n_sink"]
+    cache = {}
+    for st in SWEEP:
+        key = (tuple(st["sides"]), st["B"], st["H"], st["sets"])
+        if key not in cache:
+            cache.clear()
+            sets = []
+            for s in range(st["sets"]):
+                q, k, v = make_qkv(st["sides"], st["sides"], st["B"], st["H"], d, nf, ns, seed=s, bf16=True)
+                sets.append(tuple(torch.from_numpy(x).to(dev).to(torch.bfloat16) for x in (q, k, v)))
+                del q, k, v
+            cache[key] = sets
+        sets = cache[key]
+        B, H = st["B"], st["H"]
+        g = sv.Geometry(st["sides"], st["sides"], st["b"], ns)
+        path = SparsePath(g, st["S"], st["steps"], B, H, d, st["topk"], st["radius"])
+        info = path.info
+        stream = torch.cuda.current_stream()
+        n_ev = 2 + 2 * len(st["steps"])
+
+        def one(i, ev=None):
+            Q, K, V = sets[i % len(sets)]
+            if ev is not None:
+                ev[0].record(stream)
+            path.decision(Q, K, V)
+            if ev is not None:
+                ev[1].record(stream)
+            for j, kk in enumerate(st["steps"]):
+                path.map_step(kk)
+                if ev is not None:
+                    ev[2 + 2 * j].record(stream)
+                path.attn_step(kk, Q, K, V)
+                if ev is not None:
+                    ev[3 + 2 * j].record(stream)
+
+        for i in range(5):
+            one(i)
+        torch.cuda.synchronize()
+        n = 20
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(n)]
+        for i in range(n):
+            one(i, evs[i])
+        torch.cuda.synchronize()
+        med = lambda a, b: float(np.median([evs[i][a].elapsed_time(evs[i][b]) for i in range(n)]))
+        out = {"sweep": st["name"], "B": B, "H": H, "block": st["b"], "topk": st["topk"], "radius": st["radius"],
+               "decision_scale": st["sides"][st["S"] - 1], "decision_ms": med(0, 1), "steps": {}}
+        BH = B * H
+        for j, kk in enumerate(st["steps"]):
+            rp, ci, _ = path.csr[kk]
+            f, b_, dens, _ = sparse_accounting(rp.cpu().numpy(), ci.cpu().numpy(), info, kk, BH, d)
+            t_attn = med(2 + 2 * j, 3 + 2 * j)
+            t_map = med(1 + 2 * j, 2 + 2 * j)
+            out["steps"][str(info[kk]["h"])] = {"map_ms": t_map, "attn_ms": t_attn, "gflop": f / 1e9,
+                                                "tflops": f / t_attn / 1e9,
+                                                "frac_bf16_peak": f / t_attn / 1e9 / PEAK_BF16_TFLOPS,
+                                                "density": dens}
+        # our dense kernel at the last step, same buffers
+        kl = st["steps"][-1]
+        il = info[kl]
+        o = torch.empty(B, H, il["n_tokens"], d, dtype=torch.bfloat16, device=dev)
+
+        def dense(i):
+            Q, K, V = sets[i % len(sets)]
+            sv.sparvar_dense_attn_fwd(path.q_slice(Q, kl), path.kv_prefix(K, kl), path.kv_prefix(V, kl), o, None,
+                                      softmax_scale=path.scale)
+
+        for i in range(2):
+            dense(i)
+        torch.cuda.synchronize()
+        de = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(5)]
+        for i, (a, b_) in enumerate(de):
+            a.record(stream)
+            dense(i)
+            b_.record(stream)
+        torch.cuda.synchronize()
+        t_dense = float(np.median([a.elapsed_time(b_) for a, b_ in de]))
+        last = out["steps"][str(il["h"])]
+        out["dense_last_ms"] = t_dense
+        out["dense_last_tflops"] = 4.0 * d * BH * il["n_tokens"] * il["n_tokens_le"] / t_dense / 1e9
+        out["speedup_last_vs_own_dense"] = t_dense / last["attn_ms"]
+        print(json.dumps(out), flush=True)
+        del path
+
+
 # ---------------------------------------------------------------- main
 def main():
     args = parse()
@@ -185,6 +287,9 @@ def main():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
     dev = torch.device("cuda:0")
+    if args.sweep:
+        sweep(args, dev)
+        return
     B, H, d = CFG["B"], CFG["H"], CFG["d"]
     BH = B * H
     g = sv.Geometry(SIDES, SIDES, CFG["b"], CFG["n_sink"])

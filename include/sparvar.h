@@ -135,8 +135,9 @@ int sparvar_select_blocks(const sparvar_geometry_t* g, int32_t S, int32_t B, int
  * block scores and the per-tile top-k -- the results of sparvar_dense_attn_fwd
  * followed by sparvar_select_blocks, but for bf16 in one fused launch that
  * takes each block's probability mass from the attention pass itself (no
- * second S = Q K^T pass). fp32 inputs, tiles wider than 32 tokens or candidate
- * sets too large for the fused kernel's LDS run the two-call sequence instead.
+ * second S = Q K^T pass). fp32 inputs, tiles wider than 32 tokens, and
+ * candidate sets large enough that the per-query block masses crowd the LDS
+ * (e.g. 172 blocks at a 64x64 decision scale) run the two-call sequence.
  *   q_S: [B,H,N_S,d] (plane stride q_bh_stride); k_leS, v_leS: [B,H,N_<=S,d]
  *   (plane stride kv_bh_stride); o_S: [B,H,N_S,d] contiguous; lse_S: [B,H,N_S]
  *   fp32; scores_out: fp32 [B,H,G_S,NB_<=S]; topk_idx: int32 [B,H,G_S,topk]

@@ -265,7 +265,13 @@ int sparvar_decision_step(const sparvar_geometry_t* g, int32_t S, int32_t B, int
   const int64_t rows = (int64_t)B * H * tiles_of(T, S);
   if ((int64_t)B * H * NS >= (int64_t(1) << 31) || rows * (NB > topk ? NB : topk) >= (int64_t(1) << 31))
     return fail(SPARVAR_ERR_INVALID, "tensors too large");
-  if (dtype == SPARVAR_BF16 && decision_supported(T, S, d, NB, nullptr)) {
+  // The fused kernel keeps every query's per-block mass in LDS; when that leaves
+  // room for only one workgroup per CU (many candidate blocks), the two-call
+  // sequence is faster. SPARVAR_DECISION_FUSED: 1 = whenever supported, 0 = never.
+  size_t lds = 0;
+  const int fused = env_int("SPARVAR_DECISION_FUSED", -1);
+  const bool can_fuse = dtype == SPARVAR_BF16 && decision_supported(T, S, d, NB, &lds);
+  if (can_fuse && (fused == 1 || (fused < 0 && lds <= 80 * 1024))) {
     DecisionArgs a;
     a.G = &T;
     a.S = S;

@@ -151,6 +151,15 @@ def test_infinity_config_full_size():
              heads=[0, 17, 31], tiles_per_step=12)
 
 
+def test_schedule_2048_sampled():
+    # 2048x2048-shaped schedule: scales up to 128x128 (42521 keys), decision at
+    # 64x64 with 172 candidate blocks, top-16, steps 80/96/128. Every index list
+    # bit-exact on all 16 heads; attention and decision outputs sampled on two heads.
+    sides = INF_SIDES + [80, 96, 128]
+    run_case(sides, sides, 8, 4, 13, [14, 15, 16], 1, 16, 128, 32, 16, 1, "bf16", seed=6, heads=[0, 9],
+             tiles_per_step=12)
+
+
 # ---------------------------------------------------------------- dense kernel edge cases
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("n_q,n_kv,d", [(1, 1, 64), (33, 65, 64), (100, 333, 128), (257, 129, 128)])
