@@ -1,2 +1,3 @@
 """fp64 CPU oracle (test infrastructure only; never imported by the product path)."""
 from .sparvar_oracle import *  # noqa: F401,F403
+from .cs4a_oracle import *  # noqa: F401,F403
