@@ -156,10 +156,10 @@ def test_upsample_nearest_hand_rows_identity_and_constants():
         for a in range(n_k):
             for c in range(n_k):
                 assert up[a, c] == rows[a] * n_S + rows[c]
-    # non-square: a 2 x 3 grid onto 4 x 6 doubles both axes independently
+    # non-square with unequal ratios: a 2 x 3 grid onto 4 x 9 (rows doubled, columns tripled)
     x = np.arange(6, dtype=float)[:, None]
-    up = O.upsample_nearest(x, 2, 3, 4, 6)[:, 0].reshape(4, 6)
-    assert all(up[a, c] == (a // 2) * 3 + c // 2 for a in range(4) for c in range(6))
+    up = O.upsample_nearest(x, 2, 3, 4, 9)[:, 0].reshape(4, 9)
+    assert all(up[a, c] == (a // 2) * 3 + c // 3 for a in range(4) for c in range(9))
     x = np.random.default_rng(7).standard_normal((12, 3))
     assert np.array_equal(O.upsample_nearest(x, 3, 4, 3, 4), x)
     assert np.allclose(O.upsample_nearest(np.full((6, 2), 2.5), 2, 3, 5, 7), 2.5)
