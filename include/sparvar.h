@@ -154,6 +154,73 @@ int sparvar_decision_step(const sparvar_geometry_t* g, int32_t S, int32_t B, int
                           int32_t* topk_idx, hipStream_t stream);
 
 /*
+ * ---- Token-granular CS^4A (Sec. 3.2; appendix, Hardware-Efficient Sparse
+ * Computation and Cross-Scale Sparse Index Mapping). Query blocks are 1-D:
+ * block i of a scale holds its queries [i C, min(i C + C, N)) in flattened
+ * order, C in {32, 64, 128, 256}; G = ceil(N / C). bf16 only, d in {64, 128}.
+ *
+ * Column sums at the decision scale S: colsum[b,h,i,j] = sum over the queries
+ * q of block i of P[q,j], P = softmax(scale * Q_S K_<=S^T), using lse_S from
+ * sparvar_dense_attn_fwd (or sparvar_decision_step) at S.
+ *   q_S: [B,H,N_S,d]; k_leS: [B,H,N_<=S,d]; lse_S: [B,H,N_S] fp32;
+ *   colsum: fp32 [B,H,G_S,N_<=S].
+ */
+int sparvar_cs4a_column_sums(const sparvar_geometry_t* g, int32_t S, int32_t C, int32_t B, int32_t H,
+                             int32_t d, sparvar_dtype_t dtype, const void* q_S, int64_t q_bh_stride,
+                             const void* k_leS, int64_t k_bh_stride, const float* lse_S,
+                             float softmax_scale, float* colsum, hipStream_t stream);
+
+/*
+ * inds^(S) = TopK over each of `rows` rows of n fp32 values: the min(K, n)
+ * largest, ties to the lower index, written ascending and padded with -1.
+ *   values: [rows, n]; inds: int32 [rows, K]. 1 <= K <= 65536.
+ */
+int sparvar_cs4a_select_tokens(const float* values, int32_t rows, int32_t n, int32_t K, int32_t* inds,
+                               hipStream_t stream);
+
+/*
+ * Row stride M of the token rows of sparvar_cs4a_map_tokens: the sink tokens
+ * (all of scales 1..num_sink_scales) plus K. Host-only; < 0 on error.
+ */
+int32_t sparvar_cs4a_row_stride(const sparvar_geometry_t* g, int32_t K);
+
+/*
+ * Key tokens of every query block g of scale k (1 <= S < k <= num_scales):
+ * the sink tokens 0 .. N_sink - 1, then each token of row phi(g) of inds_S
+ * (phi(g) = floor((2g + 1) G_S / (2 G_k)), the Query Block Homography)
+ * mapped by Decompose-Align-Project -- scale l -> l' = k - (S - l), offset
+ * (u, v) -> (floor(u h_l'/h_l), floor(v w_l'/w_l)) -- dropping mapped tokens
+ * that fall among the sinks; then -1 up to the stride M. Ascending inds_S rows
+ * give ascending token rows.
+ *   inds_S: int32 [B,H,G_S,K] (sparvar_cs4a_select_tokens; -1 entries skipped);
+ *   tokens: int32 [B,H,G_k,M], M = sparvar_cs4a_row_stride(g, K).
+ */
+int sparvar_cs4a_map_tokens(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t C, int32_t B,
+                            int32_t H, int32_t K, const int32_t* inds_S, int32_t* tokens, int32_t M,
+                            hipStream_t stream);
+
+/*
+ * Gather attention over token rows at scale k: every query of block g of
+ * (b,h) attends, with one softmax, to the tokens of row (b*H + h) * G_k + g --
+ * its ids in [0, N_<=k) up to the first id outside that range (ascending ids,
+ * then padding) -- giving A; then, by mode:
+ *   0: o = A (the sparse update Delta O^(k));
+ *   1: o = base - A, base [B,H,N_k,d] (O_cache^(S) = O_dense - A at k = S);
+ *   2: o = up(base) + A, base [B,H,N_S,d] a scale-S grid (O_cache^(S)),
+ *      up() the nearest-neighbour upsampling by token centres: output token
+ *      (x, y) of scale k reads base token (floor((2x+1) h_S / (2 h_k)),
+ *      floor((2y+1) w_S / (2 w_k))) (Sec. 3.2: O^(k) = O_cache^(k) + Delta O^(k)).
+ *   q_k: [B,H,N_k,d]; k_lek, v_lek: [B,H,N_<=k,d]; o: [B,H,N_k,d] contiguous;
+ *   lse (nullable): [B,H,N_k] fp32 of A (-inf for an empty row, where A = 0);
+ *   tokens: int32 [B*H*G_k, M]. base_scale: S for mode 2, ignored otherwise.
+ */
+int sparvar_cs4a_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t C, int32_t B, int32_t H,
+                          int32_t d, sparvar_dtype_t dtype, const void* q_k, int64_t q_bh_stride,
+                          const void* k_lek, const void* v_lek, int64_t kv_bh_stride, void* o,
+                          float* lse, float softmax_scale, const int32_t* tokens, int32_t M,
+                          int32_t mode, const void* base, int32_t base_scale, hipStream_t stream);
+
+/*
  * Sink + cross-scale local blocks of every query tile of scale k (block form
  * of the CSLA mask, Sec. 3.3, and the sink set of the appendix). Row g
  * (query tile (a,c) = (g / T_w(k), g % T_w(k))) lists ascending:

@@ -298,6 +298,144 @@ int sparvar_decision_step(const sparvar_geometry_t* g, int32_t S, int32_t B, int
                                nullptr, scores_out, topk, topk_idx, stream);
 }
 
+namespace {
+int check_query_block(int32_t C) {
+  if (C != 32 && C != 64 && C != 128 && C != 256)
+    return fail(SPARVAR_ERR_UNSUPPORTED, "query block size %d is not 32, 64, 128 or 256", C);
+  return SPARVAR_OK;
+}
+}  // namespace
+
+int sparvar_cs4a_column_sums(const sparvar_geometry_t* g, int32_t S, int32_t C, int32_t B, int32_t H,
+                             int32_t d, sparvar_dtype_t dtype, const void* q_S, int64_t q_bh_stride,
+                             const void* k_leS, int64_t k_bh_stride, const float* lse_S,
+                             float softmax_scale, float* colsum, hipStream_t stream) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if (S < 1 || S > T.L) return fail(SPARVAR_ERR_INVALID, "decision scale %d outside [1, %d]", S, T.L);
+  if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
+  if ((st = check_dtype_d(dtype, d))) return st;
+  if (dtype != SPARVAR_BF16) return fail(SPARVAR_ERR_UNSUPPORTED, "token-granular paths take bf16 inputs");
+  if ((st = check_query_block(C))) return st;
+  if (!lse_S || !colsum) return fail(SPARVAR_ERR_INVALID, "lse_S and colsum are required");
+  if (!(std::isfinite(softmax_scale))) return fail(SPARVAR_ERR_INVALID, "softmax_scale is not finite");
+  const int32_t NS = T.h[S - 1] * T.w[S - 1];
+  if ((st = check_plane(q_S, q_bh_stride, NS, d, 2, "q_S"))) return st;
+  if ((st = check_plane(k_leS, k_bh_stride, T.C[S], d, 2, "k_leS"))) return st;
+  const int64_t G = (NS + C - 1) / C;
+  if ((int64_t)B * H * G * T.C[S] >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "column-sum tensor too large");
+  Cs4aColsumArgs a;
+  a.BH = B * H;
+  a.n_q = NS;
+  a.n_kv = T.C[S];
+  a.d = d;
+  a.C = C;
+  a.q = q_S;
+  a.k = k_leS;
+  a.lse = lse_S;
+  a.out = colsum;
+  a.q_bh_stride = q_bh_stride;
+  a.k_bh_stride = k_bh_stride;
+  a.softmax_scale = softmax_scale;
+  a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
+  return hip_status(launch_cs4a_colsum(a, stream), "column-sum launch");
+}
+
+int sparvar_cs4a_select_tokens(const float* values, int32_t rows, int32_t n, int32_t K, int32_t* inds,
+                               hipStream_t stream) {
+  if (!values || !inds) return fail(SPARVAR_ERR_INVALID, "values and inds are required");
+  if (rows < 0 || n < 1) return fail(SPARVAR_ERR_INVALID, "rows must be >= 0 and n >= 1");
+  if (K < 1 || K > 65536) return fail(SPARVAR_ERR_INVALID, "K %d outside [1, 65536]", K);
+  if ((int64_t)rows * n >= (int64_t(1) << 31) || (int64_t)rows * K >= (int64_t(1) << 31))
+    return fail(SPARVAR_ERR_INVALID, "tensors too large");
+  return hip_status(launch_cs4a_topk(values, rows, n, K, inds, stream), "token top-K launch");
+}
+
+int32_t sparvar_cs4a_row_stride(const sparvar_geometry_t* g, int32_t K) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if (K < 1 || K > 65536) return fail(SPARVAR_ERR_INVALID, "K %d outside [1, 65536]", K);
+  ok();
+  return T.C[T.n_sink] + K;
+}
+
+int sparvar_cs4a_map_tokens(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t C, int32_t B,
+                            int32_t H, int32_t K, const int32_t* inds_S, int32_t* tokens, int32_t M,
+                            hipStream_t stream) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if (!(1 <= S && S < k && k <= T.L)) return fail(SPARVAR_ERR_INVALID, "need 1 <= S < k <= %d", T.L);
+  if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
+  if ((st = check_query_block(C))) return st;
+  if (K < 1 || K > 65536) return fail(SPARVAR_ERR_INVALID, "K %d outside [1, 65536]", K);
+  if (!inds_S || !tokens) return fail(SPARVAR_ERR_INVALID, "inds_S and tokens are required");
+  if (M < T.C[T.n_sink] + K) return fail(SPARVAR_ERR_CAPACITY, "row stride %d < %d", M, T.C[T.n_sink] + K);
+  const int64_t Gk = (T.h[k - 1] * T.w[k - 1] + C - 1) / C;
+  if ((int64_t)B * H * Gk * M >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "token rows too large");
+  return hip_status(launch_cs4a_map(T, S, k, B * H, C, K, inds_S, tokens, M, stream), "token mapping launch");
+}
+
+int sparvar_cs4a_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t C, int32_t B, int32_t H,
+                          int32_t d, sparvar_dtype_t dtype, const void* q_k, int64_t q_bh_stride,
+                          const void* k_lek, const void* v_lek, int64_t kv_bh_stride, void* o,
+                          float* lse, float softmax_scale, const int32_t* tokens, int32_t M,
+                          int32_t mode, const void* base, int32_t base_scale, hipStream_t stream) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if (k < 1 || k > T.L) return fail(SPARVAR_ERR_INVALID, "scale %d outside [1, %d]", k, T.L);
+  if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
+  if ((st = check_dtype_d(dtype, d))) return st;
+  if (dtype != SPARVAR_BF16) return fail(SPARVAR_ERR_UNSUPPORTED, "token-granular paths take bf16 inputs");
+  if ((st = check_query_block(C))) return st;
+  if (!tokens || M < 1) return fail(SPARVAR_ERR_INVALID, "tokens and a row stride >= 1 are required");
+  if (mode < 0 || mode > 2) return fail(SPARVAR_ERR_INVALID, "mode %d is not 0, 1 or 2", mode);
+  if (!(std::isfinite(softmax_scale))) return fail(SPARVAR_ERR_INVALID, "softmax_scale is not finite");
+  const int32_t Nk = T.h[k - 1] * T.w[k - 1];
+  if ((int64_t)B * H * Nk >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "B*H*N_k too large");
+  if ((st = check_plane(q_k, q_bh_stride, Nk, d, 2, "q_k"))) return st;
+  if ((st = check_plane(k_lek, kv_bh_stride, T.C[k], d, 2, "k_lek"))) return st;
+  if ((st = check_plane(v_lek, kv_bh_stride, T.C[k], d, 2, "v_lek"))) return st;
+  if ((st = check_plane(o, (int64_t)Nk * d, Nk, d, 2, "o"))) return st;
+  const int64_t Gk = (Nk + C - 1) / C;
+  if ((int64_t)B * H * Gk * M >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "token rows too large");
+  TokenAttnArgs a;
+  a.up_hs = a.up_ws = a.up_hk = a.up_wk = 1;
+  if (mode == 1) {
+    if ((st = check_plane(base, (int64_t)Nk * d, Nk, d, 2, "base"))) return st;
+  } else if (mode == 2) {
+    if (base_scale < 1 || base_scale > k) return fail(SPARVAR_ERR_INVALID, "base scale %d outside [1, %d]", base_scale, k);
+    const int32_t NS = T.h[base_scale - 1] * T.w[base_scale - 1];
+    if ((st = check_plane(base, (int64_t)NS * d, NS, d, 2, "base"))) return st;
+    a.up_hs = T.h[base_scale - 1];
+    a.up_ws = T.w[base_scale - 1];
+    a.up_hk = T.h[k - 1];
+    a.up_wk = T.w[k - 1];
+  }
+  a.BH = B * H;
+  a.n_q = Nk;
+  a.n_kv = T.C[k];
+  a.d = d;
+  a.C = C;
+  a.M = M;
+  a.q = q_k;
+  a.k = k_lek;
+  a.v = v_lek;
+  a.o = o;
+  a.lse = lse;
+  a.q_bh_stride = q_bh_stride;
+  a.kv_bh_stride = kv_bh_stride;
+  a.softmax_scale = softmax_scale;
+  a.tokens = tokens;
+  a.epi_mode = mode;
+  a.epi_base = mode == 0 ? nullptr : base;
+  a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
+  return hip_status(launch_token_attn(a, stream), "token attention launch");
+}
+
 int64_t sparvar_local_blocks_capacity(const sparvar_geometry_t* g, int32_t k, int32_t radius,
                                       int32_t prev_dilation) {
   GeoTable T;

@@ -35,6 +35,14 @@ struct AttnIO {
   int32_t n_items;       // workgroups doing work
   int32_t swizzle;       // remap workgroups so consecutive items share an XCD
   float scale_log2;      // softmax_scale * log2(e)
+  // Epilogue (bf16 kernel): 0 writes the attention output A; 1 writes base - A
+  // (base: [planes, o_rows, D], same layout as o); 2 writes up(base) + A, where
+  // up() takes for output row (x, y) of an up_hk x up_wk grid the base row
+  // (floor((2x+1) up_hs / (2 up_hk)), floor((2y+1) up_ws / (2 up_wk))) of an
+  // up_hs x up_ws grid (base: [planes, up_hs * up_ws, D]).
+  int32_t epi_mode = 0;
+  const void* epi_base = nullptr;
+  int32_t up_hs = 1, up_ws = 1, up_hk = 1, up_wk = 1;
 };
 
 // Queries of one workgroup: slot i in [q0, q1) is plane row
@@ -60,6 +68,7 @@ template <int KC>
 struct DenseSrc {
   static constexpr bool kSparse = false;
   static constexpr bool kGrouped = false;
+  static constexpr bool kTokens = false;
   int32_t n_q, n_kv, slabs, q_per_wg;
   template <int NT>
   static constexpr int table_bytes() { return 16; }
@@ -77,6 +86,64 @@ struct DenseSrc {
     return s;
   }
   __device__ __forceinline__ DenseCursor<KC> cursor(int32_t) const { return DenseCursor<KC>{0, n_kv}; }
+};
+
+// Key tokens listed one by one (token-granular rows): chunk slot r holds the
+// token tokens[base + r].
+template <int KC>
+struct TokenCursor {
+  int32_t pos, len, row_off;
+  __device__ __forceinline__ bool next(Chunk& c) {
+    if (pos >= len) return false;
+    const int32_t cnt = (len - pos < KC) ? len - pos : KC;
+    c = run_chunk(row_off + pos, cnt);
+    pos += cnt;
+    return true;
+  }
+};
+
+// Rows of key tokens for 1-D query blocks of C contiguous queries (C = 32 NW):
+// row r = (b*H + h) * n_blocks + g lists, for the queries [g C, g C + C) of the
+// plane, ascending token ids in [0, n_kv) followed by padding (any id outside
+// that range), at a fixed stride M.
+template <int KC>
+struct TokenSrc {
+  static constexpr bool kSparse = false;
+  static constexpr bool kGrouped = false;
+  static constexpr bool kTokens = true;
+  const int32_t* tokens;
+  int32_t M, C, n_q, n_kv, n_blocks;
+  template <int NT>
+  static constexpr int table_bytes() { return 64; }
+  __device__ __forceinline__ int tile_of(int) const { return 0; }
+  __device__ __forceinline__ QuerySet queries(int32_t item, int wave) const {
+    QuerySet s;
+    s.bh = item / n_blocks;
+    const int32_t g = item - s.bh * n_blocks;
+    s.qbase = g * C;
+    s.qnc = 1 << 30;  // contiguous rows
+    s.qstride = 0;
+    s.q0 = wave * kQPerWave;
+    s.q1 = (n_q - g * C < C) ? n_q - g * C : C;
+    return s;
+  }
+  // The row's token count (its ids up to the first padding entry), by the whole workgroup.
+  template <int NT>
+  __device__ __forceinline__ TokenCursor<KC> token_cursor(int32_t item, char* lds) const {
+    const int32_t* row = tokens + (int64_t)item * M;
+    int32_t cnt = 0;
+    for (int32_t i = threadIdx.x; i < M; i += NT) {
+      const int32_t t = row[i];
+      cnt += (t >= 0 && t < n_kv) ? 1 : 0;
+    }
+    int32_t total;
+    block_excl_scan<NT>(cnt, reinterpret_cast<int32_t*>(lds), total);
+    TokenCursor<KC> c;
+    c.pos = 0;
+    c.len = __builtin_amdgcn_readfirstlane(total);
+    c.row_off = item * M;
+    return c;
+  }
 };
 
 // Walks the kept blocks of one CSR row as chunks of at most KC keys.
@@ -313,6 +380,7 @@ template <int KC>
 struct SparseSrc {
   static constexpr bool kSparse = true;
   static constexpr bool kGrouped = false;
+  static constexpr bool kTokens = false;
   GeoTable G;
   const int32_t* row_ptr;
   const int32_t* col_idx;
@@ -543,6 +611,7 @@ template <int KC>
 struct GroupSrc {
   static constexpr bool kSparse = true;
   static constexpr bool kGrouped = true;
+  static constexpr bool kTokens = false;
   GeoTable G;
   const int32_t* row_ptr;
   const int32_t* col_idx;
@@ -727,7 +796,10 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
     for (int j = 0; j < kLoads; ++j) {
       const int first = (j * NW + wave_s) * 64;
       const int r = ld_row[j];
-      const uint32_t off = (uint32_t)(chunk_token(c, r < c.count ? r : 0) * D + 8 * ld_unit[j]) * 2u;
+      int32_t tok;
+      if constexpr (Src::kTokens) tok = src.tokens[c.base + (r < c.count ? r : 0)];
+      else tok = chunk_token(c, r < c.count ? r : 0);
+      const uint32_t off = (uint32_t)(tok * D + 8 * ld_unit[j]) * 2u;
       dma16(kbytes + off, kb + first * 16);
       dma16(vbytes + off, kb + kTile + first * 16);
     }
@@ -736,6 +808,8 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
   auto cur = [&]() {
     if constexpr (Src::kSparse) {
       return src.template table_cursor<NT>(item, tsmem);
+    } else if constexpr (Src::kTokens) {
+      return src.template token_cursor<NT>(item, tsmem);
     } else {
       return src.cursor(item);
     }
@@ -876,14 +950,36 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
   if (qvalid) {
     const int64_t orow = (int64_t)qs.bh * io.o_rows + qrow;
     bf16_bits* op = static_cast<bf16_bits*>(io.o) + orow * D;
+    const bf16_bits* bp = nullptr;  // epilogue base row
+    float sgn = 1.f;
+    if (io.epi_mode == 1) {
+      bp = static_cast<const bf16_bits*>(io.epi_base) + orow * D;
+      sgn = -1.f;
+    } else if (io.epi_mode == 2) {
+      const int32_t x = qrow / io.up_wk, y = qrow - (qrow / io.up_wk) * io.up_wk;
+      const int32_t xs = ((2 * x + 1) * io.up_hs) / (2 * io.up_hk);
+      const int32_t ys = ((2 * y + 1) * io.up_ws) / (2 * io.up_wk);
+      bp = static_cast<const bf16_bits*>(io.epi_base) +
+           ((int64_t)qs.bh * io.up_hs * io.up_ws + xs * io.up_ws + ys) * D;
+    }
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int d = 32 * dt + 8 * j + 4 * half;
+        float r[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) r[e] = acc[dt][4 * j + e] * inv * sgn;
+        if (bp) {
+          const uint2 b = *reinterpret_cast<const uint2*>(bp + d);
+          r[0] += __uint_as_float(b.x << 16);
+          r[1] += __uint_as_float(b.x & 0xffff0000u);
+          r[2] += __uint_as_float(b.y << 16);
+          r[3] += __uint_as_float(b.y & 0xffff0000u);
+        }
         uint2 w;
-        w.x = pack_bf16x2(acc[dt][4 * j + 0] * inv, acc[dt][4 * j + 1] * inv);
-        w.y = pack_bf16x2(acc[dt][4 * j + 2] * inv, acc[dt][4 * j + 3] * inv);
+        w.x = pack_bf16x2(r[0], r[1]);
+        w.y = pack_bf16x2(r[2], r[3]);
         *reinterpret_cast<uint2*>(op + d) = w;
       }
     }
@@ -1143,6 +1239,48 @@ hipError_t launch_dense_attn(const DenseAttnArgs& a, hipStream_t stream) {
     return s;
   };
   return dispatch<DenseSrc>(a.bf16, a.d, nw, kc, ns, io, make, stream);
+}
+
+// token-row launch shapes (d, waves = C / 32, keys per chunk), two stages
+#define SV_TOKEN_SHAPES(X) \
+  X(128, 1, 64) X(128, 2, 64) X(128, 4, 64) X(128, 8, 64) X(64, 1, 64) X(64, 2, 64) X(64, 4, 64) X(64, 8, 64)
+
+hipError_t launch_token_attn(const TokenAttnArgs& a, hipStream_t stream) {
+  const int nw = a.C / kQPerWave;
+  AttnIO io;
+  io.q = a.q;
+  io.k = a.k;
+  io.v = a.v;
+  io.o = a.o;
+  io.lse = a.lse;
+  io.q_bh_stride = a.q_bh_stride;
+  io.kv_bh_stride = a.kv_bh_stride;
+  io.o_rows = a.n_q;
+  const int32_t n_blocks = (a.n_q + a.C - 1) / a.C;
+  io.n_items = a.BH * n_blocks;
+  io.swizzle = a.swizzle;
+  io.scale_log2 = a.softmax_scale * kLog2e;
+  io.epi_mode = a.epi_mode;
+  io.epi_base = a.epi_base;
+  io.up_hs = a.up_hs;
+  io.up_ws = a.up_ws;
+  io.up_hk = a.up_hk;
+  io.up_wk = a.up_wk;
+  auto make = [&](auto proto) {
+    auto s = proto;
+    s.tokens = a.tokens;
+    s.M = a.M;
+    s.C = a.C;
+    s.n_q = a.n_q;
+    s.n_kv = a.n_kv;
+    s.n_blocks = n_blocks;
+    return s;
+  };
+#define SV_TOK(DD, NN, KK) \
+  if (a.d == DD && nw == NN) return launch_bf16<DD, NN, KK, 2>(io, make(TokenSrc<KK>{}), stream);
+  SV_TOKEN_SHAPES(SV_TOK)
+#undef SV_TOK
+  return hipErrorInvalidValue;
 }
 
 namespace {

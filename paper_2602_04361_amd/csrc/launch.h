@@ -68,7 +68,36 @@ struct DecisionArgs {
   int swizzle;
 };
 
+struct Cs4aColsumArgs {
+  int32_t BH, n_q, n_kv, d, C;
+  const void *q, *k;
+  const float* lse;
+  float* out;
+  int64_t q_bh_stride, k_bh_stride;
+  float softmax_scale;
+  int swizzle;
+};
+
+struct TokenAttnArgs {
+  int32_t BH, n_q, n_kv, d, C, M;
+  const void *q, *k, *v;
+  void* o;
+  float* lse;
+  int64_t q_bh_stride, kv_bh_stride;
+  float softmax_scale;
+  const int32_t* tokens;
+  int epi_mode;
+  const void* epi_base;
+  int32_t up_hs, up_ws, up_hk, up_wk;
+  int swizzle;
+};
+
 hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream);
+hipError_t launch_token_attn(const TokenAttnArgs& a, hipStream_t stream);
+hipError_t launch_cs4a_colsum(const Cs4aColsumArgs& a, hipStream_t stream);
+hipError_t launch_cs4a_topk(const float* in, int32_t rows, int32_t n, int32_t K, int32_t* out, hipStream_t stream);
+hipError_t launch_cs4a_map(const GeoTable& G, int S, int k, int32_t BH, int32_t C, int32_t K, const int32_t* inds,
+                           int32_t* tokens, int32_t M, hipStream_t stream);
 // fused dense attention + LSE + pooled scores + top-k at the decision scale (bf16)
 bool decision_supported(const GeoTable& G, int S, int d, int32_t NB, size_t* lds_bytes);
 hipError_t launch_decision(const DecisionArgs& a, hipStream_t stream);

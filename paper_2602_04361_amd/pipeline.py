@@ -101,3 +101,70 @@ class SparsePath:
         self.decision(Q_all, K_all, V_all)
         for k in self.steps:
             self.step(k, Q_all, K_all, V_all)
+
+
+class Cs4aPath:
+    """One layer of the token-granular CS^4A path (Sec. 3.2) as C-ABI calls.
+
+    decision(): dense attention with LSE at S, column sums over 1-D query blocks
+                of C queries, the top-K tokens of each block, and O_cache at S
+                (O_dense minus the attention restricted to those tokens);
+    step(k):    the token rows of scale k (sinks + mapped tokens), then the
+                gather attention, adding the upsampled O_cache unless
+                with_cache is False.
+    """
+
+    def __init__(self, geom: sv.Geometry, S, steps, B, H, d, C, K, device="cuda", softmax_scale=None,
+                 with_cache=True):
+        self.g = geom
+        self.S, self.steps = int(S), [int(k) for k in steps]
+        self.B, self.H, self.d, self.C, self.K = B, H, d, C, K
+        self.with_cache = with_cache
+        self.scale = float(torch.tensor(1.0 / math.sqrt(d), dtype=torch.float32)) if softmax_scale is None \
+            else float(softmax_scale)
+        info = {l: geom.scale_info(l) for l in range(1, len(geom.h) + 1)}
+        self.info = info
+        iS = info[S]
+        G_S = -(-iS["n_tokens"] // C)
+        bf = dict(dtype=torch.bfloat16, device=device)
+        self.o_S = torch.empty(B, H, iS["n_tokens"], d, **bf)
+        self.lse_S = torch.empty(B, H, iS["n_tokens"], dtype=torch.float32, device=device)
+        self.colsum = torch.empty(B, H, G_S, iS["n_tokens_le"], dtype=torch.float32, device=device)
+        self.inds = torch.empty(B, H, G_S, K, dtype=torch.int32, device=device)
+        self.o_cache = torch.empty(B, H, iS["n_tokens"], d, **bf)
+        self.M = sv.sparvar_cs4a_row_stride(geom, K)
+        self.tokens, self.out = {}, {}
+        for k in self.steps:
+            G_k = -(-info[k]["n_tokens"] // C)
+            self.tokens[k] = torch.empty(B, H, G_k, self.M, dtype=torch.int32, device=device)
+            self.out[k] = torch.empty(B, H, info[k]["n_tokens"], d, **bf)
+
+    def q_slice(self, Q_all, l):
+        i = self.info[l]
+        return Q_all[:, :, i["token_offset"]:i["n_tokens_le"]]
+
+    def kv_prefix(self, X_all, l):
+        return X_all[:, :, :self.info[l]["n_tokens_le"]]
+
+    def decision(self, Q_all, K_all, V_all):
+        S = self.S
+        q, kk, vv = self.q_slice(Q_all, S), self.kv_prefix(K_all, S), self.kv_prefix(V_all, S)
+        sv.sparvar_dense_attn_fwd(q, kk, vv, self.o_S, self.lse_S, softmax_scale=self.scale)
+        sv.sparvar_cs4a_column_sums(self.g, S, self.C, q, kk, self.lse_S, self.colsum, softmax_scale=self.scale)
+        sv.sparvar_cs4a_select_tokens(self.colsum, self.K, self.inds)
+        if self.with_cache:
+            sv.sparvar_cs4a_attn_fwd(self.g, S, self.C, q, kk, vv, self.o_cache, self.inds, self.K, mode=1,
+                                     base=self.o_S, softmax_scale=self.scale)
+
+    def step(self, k, Q_all, K_all, V_all):
+        sv.sparvar_cs4a_map_tokens(self.g, self.S, k, self.C, self.B, self.H, self.K, self.inds, self.tokens[k],
+                                   self.M)
+        sv.sparvar_cs4a_attn_fwd(self.g, k, self.C, self.q_slice(Q_all, k), self.kv_prefix(K_all, k),
+                                 self.kv_prefix(V_all, k), self.out[k], self.tokens[k], self.M,
+                                 mode=2 if self.with_cache else 0, base=self.o_cache if self.with_cache else None,
+                                 base_scale=self.S, softmax_scale=self.scale)
+
+    def run(self, Q_all, K_all, V_all):
+        self.decision(Q_all, K_all, V_all)
+        for k in self.steps:
+            self.step(k, Q_all, K_all, V_all)

@@ -23,6 +23,11 @@ EXPORTS = [
     "sparvar_dense_attn_fwd",
     "sparvar_select_blocks",
     "sparvar_decision_step",
+    "sparvar_cs4a_column_sums",
+    "sparvar_cs4a_select_tokens",
+    "sparvar_cs4a_row_stride",
+    "sparvar_cs4a_map_tokens",
+    "sparvar_cs4a_attn_fwd",
     "sparvar_local_blocks_capacity",
     "sparvar_local_blocks",
     "sparvar_map_index_capacity",
@@ -76,6 +81,13 @@ def load_library(path: str = LIB_PATH):
                                                  vp, i32, vp, vp]),
         "sparvar_decision_step": (ctypes.c_int, [G, i32, i32, i32, i32, ctypes.c_int, vp, i64, vp, vp, i64, vp, vp,
                                                  f32, vp, i32, vp, vp]),
+        "sparvar_cs4a_column_sums": (ctypes.c_int, [G, i32, i32, i32, i32, i32, ctypes.c_int, vp, i64, vp, i64, vp,
+                                                    f32, vp, vp]),
+        "sparvar_cs4a_select_tokens": (ctypes.c_int, [vp, i32, i32, i32, vp, vp]),
+        "sparvar_cs4a_row_stride": (i32, [G, i32]),
+        "sparvar_cs4a_map_tokens": (ctypes.c_int, [G, i32, i32, i32, i32, i32, i32, vp, vp, i32, vp]),
+        "sparvar_cs4a_attn_fwd": (ctypes.c_int, [G, i32, i32, i32, i32, i32, ctypes.c_int, vp, i64, vp, vp, i64, vp,
+                                                 vp, f32, vp, i32, i32, vp, i32, vp]),
         "sparvar_local_blocks_capacity": (i64, [G, i32, i32, i32]),
         "sparvar_local_blocks": (ctypes.c_int, [G, i32, i32, i32, vp, vp, i64, vp]),
         "sparvar_map_index_capacity": (i64, [G, i32, i32, i32, i32, i32, i32, i32]),
@@ -208,6 +220,54 @@ def sparvar_decision_step(geom, S, q_S, k_leS, v_leS, o_S, lse_S, scores_out, to
                                      _scale(softmax_scale, d), _ptr(scores_out), topk, _ptr(topk_idx),
                                      _stream(stream)))
     return topk_idx
+
+
+def sparvar_cs4a_column_sums(geom, S, C, q_S, k_leS, lse_S, colsum, softmax_scale=None, stream=None):
+    """Token column sums over 1-D query blocks of C queries at S; see sparvar.h."""
+    lib = load_library()
+    B, H, _, d = q_S.shape
+    _check(lib.sparvar_cs4a_column_sums(geom.ref, S, C, B, H, d, _dtype_code(q_S), _ptr(q_S), _plane_stride(q_S, "q_S"),
+                                        _ptr(k_leS), _plane_stride(k_leS, "k_leS"), _ptr(lse_S),
+                                        _scale(softmax_scale, d), _ptr(colsum), _stream(stream)))
+    return colsum
+
+
+def sparvar_cs4a_select_tokens(values, K, inds, stream=None):
+    """Top-K per row of values [..., n] into inds [..., K]; see sparvar.h."""
+    n = values.shape[-1]
+    rows = values.numel() // n
+    if not values.is_contiguous() or not inds.is_contiguous() or inds.numel() != rows * K:
+        raise SparvarError(ERR_INVALID, "values and inds must be contiguous [rows, n] and [rows, K]")
+    _check(load_library().sparvar_cs4a_select_tokens(_ptr(values), rows, n, K, _ptr(inds), _stream(stream)))
+    return inds
+
+
+def sparvar_cs4a_row_stride(geom, K):
+    m = load_library().sparvar_cs4a_row_stride(geom.ref, K)
+    if m < 0:
+        _check(int(m))
+    return int(m)
+
+
+def sparvar_cs4a_map_tokens(geom, S, k, C, B, H, K, inds_S, tokens, M, stream=None):
+    """Sink tokens + mapped top-K tokens for every query block of scale k; see sparvar.h."""
+    _check(load_library().sparvar_cs4a_map_tokens(geom.ref, S, k, C, B, H, K, _ptr(inds_S), _ptr(tokens), M,
+                                                  _stream(stream)))
+    return tokens
+
+
+def sparvar_cs4a_attn_fwd(geom, k, C, q_k, k_lek, v_lek, o, tokens, M, lse=None, mode=0, base=None, base_scale=0,
+                          softmax_scale=None, stream=None):
+    """Gather attention over token rows (mode 0), O_cache (1) or O_cache upsampled + sparse update (2)."""
+    lib = load_library()
+    B, H, _, d = q_k.shape
+    if _plane_stride(v_lek, "v_lek") != _plane_stride(k_lek, "k_lek"):
+        raise SparvarError(ERR_INVALID, "k_lek and v_lek must share one plane stride")
+    _check(lib.sparvar_cs4a_attn_fwd(geom.ref, k, C, B, H, d, _dtype_code(q_k), _ptr(q_k), _plane_stride(q_k, "q_k"),
+                                     _ptr(k_lek), _ptr(v_lek), _plane_stride(k_lek, "k_lek"), _ptr(o), _ptr(lse),
+                                     _scale(softmax_scale, d), _ptr(tokens), M, mode, _ptr(base), base_scale,
+                                     _stream(stream)))
+    return o
 
 
 def sparvar_local_blocks_capacity(geom, k, radius, prev_dilation=0):

@@ -17,7 +17,7 @@ INF = [1, 2, 4, 6, 8, 12, 16, 20, 24, 32, 40, 48, 64]
 def declared_symbols():
     with open(os.path.join(ROOT, "include", "sparvar.h")) as f:
         text = f.read()
-    return sorted(set(re.findall(r"^\s*(?:const\s+char\s*\*|int64_t|int)\s+(sparvar_\w+)\s*\(", text, re.M)))
+    return sorted(set(re.findall(r"^\s*(?:const\s+char\s*\*|int64_t|int32_t|int)\s+(sparvar_\w+)\s*\(", text, re.M)))
 
 
 def test_library_exports_every_declared_symbol():
