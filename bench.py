@@ -269,6 +269,82 @@ def sweep(args, dev):
         del path
 
 
+CS4A_SWEEP = [dict(C=128, K=1024), dict(C=128, K=512), dict(C=64, K=1024), dict(C=256, K=1024)]
+
+
+def sweep_cs4a(dev):
+    """Token-granular CS^4A path on the Infinity layer: per-stage times and the
+    gather attention's algorithmic TFLOP/s (4 d * queries * kept tokens)."""
+    import torch
+
+    from paper_2602_04361_amd import sparvar as sv
+    from paper_2602_04361_amd.pipeline import Cs4aPath
+    from paper_2602_04361_amd.synth import make_qkv
+
+    B, H, d = CFG["B"], CFG["H"], CFG["d"]
+    sets = []
+    for s in range(N_SETS):
+        q, k, v = make_qkv(SIDES, SIDES, B, H, d, CFG["n_freq"], CFG["n_sink"], seed=s, bf16=True)
+        sets.append(tuple(torch.from_numpy(x).to(dev).to(torch.bfloat16) for x in (q, k, v)))
+    g = sv.Geometry(SIDES, SIDES, CFG["b"], CFG["n_sink"])
+    stream = torch.cuda.current_stream()
+    for st in CS4A_SWEEP:
+        path = Cs4aPath(g, CFG["S"], CFG["steps"], B, H, d, st["C"], st["K"])
+        names = ["dense_S", "colsum", "topk", "cache"] + [f"{n}_{k}" for k in CFG["steps"] for n in ("map", "attn")]
+
+        def one(i, ev=None):
+            Q, K, V = sets[i % len(sets)]
+            S = CFG["S"]
+            q, kk, vv = path.q_slice(Q, S), path.kv_prefix(K, S), path.kv_prefix(V, S)
+            rec = (lambda j: ev[j].record(stream)) if ev is not None else (lambda j: None)
+            rec(0)
+            sv.sparvar_dense_attn_fwd(q, kk, vv, path.o_S, path.lse_S, softmax_scale=path.scale)
+            rec(1)
+            sv.sparvar_cs4a_column_sums(g, S, path.C, q, kk, path.lse_S, path.colsum, softmax_scale=path.scale)
+            rec(2)
+            sv.sparvar_cs4a_select_tokens(path.colsum, path.K, path.inds)
+            rec(3)
+            sv.sparvar_cs4a_attn_fwd(g, S, path.C, q, kk, vv, path.o_cache, path.inds, path.K, mode=1, base=path.o_S,
+                                     softmax_scale=path.scale)
+            rec(4)
+            j = 5
+            for kk_ in CFG["steps"]:
+                sv.sparvar_cs4a_map_tokens(g, S, kk_, path.C, B, H, path.K, path.inds, path.tokens[kk_], path.M)
+                rec(j)
+                sv.sparvar_cs4a_attn_fwd(g, kk_, path.C, path.q_slice(Q, kk_), path.kv_prefix(K, kk_),
+                                         path.kv_prefix(V, kk_), path.out[kk_], path.tokens[kk_], path.M, mode=2,
+                                         base=path.o_cache, base_scale=S, softmax_scale=path.scale)
+                rec(j + 1)
+                j += 2
+
+        for i in range(5):
+            one(i)
+        torch.cuda.synchronize()
+        n = 20
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)] for _ in range(n)]
+        for i in range(n):
+            one(i, evs[i])
+        torch.cuda.synchronize()
+        med = {nm: float(np.median([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(n)]))
+               for j, nm in enumerate(names)}
+        out = {"sweep": f"cs4a_C{st['C']}_K{st['K']}", "B": B, "H": H, "C": st["C"], "K": st["K"],
+               "stages_ms": {nm: med[nm] for nm in ("dense_S", "colsum", "topk", "cache")}, "steps": {}}
+        for kk_ in CFG["steps"]:
+            toks = path.tokens[kk_].cpu().numpy().reshape(B * H, -1, path.M)
+            n_q = path.info[kk_]["n_tokens"]
+            blocks = -(-n_q // st["C"])
+            qsz = np.array([min(st["C"], n_q - i * st["C"]) for i in range(blocks)])
+            kept = ((toks >= 0) & (toks < path.info[kk_]["n_tokens_le"])).sum(axis=2)
+            flops = 4.0 * d * float((kept * qsz[None, :]).sum())
+            t = med[f"attn_{kk_}"]
+            out["steps"][str(path.info[kk_]["h"])] = {
+                "map_ms": med[f"map_{kk_}"], "attn_ms": t, "gflop": flops / 1e9, "tflops": flops / t / 1e9,
+                "frac_bf16_peak": flops / t / 1e9 / PEAK_BF16_TFLOPS,
+                "density": float((kept * qsz[None, :]).sum()) / (B * H * n_q * path.info[kk_]["n_tokens_le"])}
+        print(json.dumps(out), flush=True)
+        del path
+
+
 # ---------------------------------------------------------------- main
 def main():
     args = parse()
@@ -289,6 +365,7 @@ def main():
     dev = torch.device("cuda:0")
     if args.sweep:
         sweep(args, dev)
+        sweep_cs4a(dev)
         return
     B, H, d = CFG["B"], CFG["H"], CFG["d"]
     BH = B * H
