@@ -205,16 +205,19 @@ __global__ __launch_bounds__(kTopkThreads) void cs4a_topk_kernel(const float* __
 }
 
 // ---------------------------------------------------------------- token mapping
-// One wave per target row r = (b*H + h) * G_k + g: the sink tokens 0 .. n_sink - 1,
-// then every listed token j of source row phi(g) mapped to step k (tokens that
-// land among the sinks are dropped), then -1 up to the row stride M. Listed
-// tokens ascending give ascending rows (the map is increasing in j).
+// One workgroup per target row r = (b*H + h) * G_k + g: the sink tokens
+// 0 .. n_sink - 1, then every listed token j of source row phi(g) mapped to step
+// k (tokens that land among the sinks are dropped), kept in list order by a
+// workgroup prefix count, then -1 up to the row stride M. Listed tokens
+// ascending give ascending rows (the map is increasing in j).
 struct MapTokIO {
   GeoTable G;
   const int32_t* inds;  // [planes, G_S, K]
   int32_t* tokens;      // [planes, G_k, M]
   int32_t S, k, K, M, G_S, G_k, n_sink_tok, rows;
 };
+
+constexpr int kMapThreads = 256;
 
 __device__ __forceinline__ int32_t map_token(const GeoTable& G, int32_t j, int S, int k) {
   int l = 1;
@@ -227,10 +230,12 @@ __device__ __forceinline__ int32_t map_token(const GeoTable& G, int32_t j, int S
   return G.C[lp - 1] + up * G.w[lp - 1] + vp;
 }
 
-__global__ __launch_bounds__(64) void cs4a_map_kernel(MapTokIO io) {
+__global__ __launch_bounds__(kMapThreads) void cs4a_map_kernel(MapTokIO io) {
+  constexpr int NT = kMapThreads;
+  __shared__ int32_t wt[NT / 64];
   const int32_t r = blockIdx.x;
   if (r >= io.rows) return;
-  const int lane = threadIdx.x;
+  const int tid = threadIdx.x;
   const int32_t bh = r / io.G_k;
   const int32_t g = r - bh * io.G_k;
   const int32_t src = (int32_t)(((int64_t)(2 * g + 1) * io.G_S) / (2 * (int64_t)io.G_k));
@@ -238,20 +243,20 @@ __global__ __launch_bounds__(64) void cs4a_map_kernel(MapTokIO io) {
   int32_t* out = io.tokens + (int64_t)r * io.M;
   const int32_t ns = io.n_sink_tok;
   const int32_t n_le_S = io.G.C[io.S];
-  for (int32_t i = lane; i < ns; i += 64) out[i] = i;
+  for (int32_t i = tid; i < ns; i += NT) out[i] = i;
   int32_t pos = ns;
-  for (int32_t base = 0; base < io.K; base += 64) {
-    const int32_t i = base + lane;
+  for (int32_t base = 0; base < io.K; base += NT) {
+    const int32_t i = base + tid;
     const int32_t j = i < io.K ? in[i] : -1;
     int32_t m = -1;
     if (j >= 0 && j < n_le_S) m = map_token(io.G, j, io.S, io.k);
-    const bool keep = m >= ns;
-    const uint64_t bal = __builtin_amdgcn_ballot_w64(keep);
-    const int32_t before = __builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0));
+    const int32_t keep = m >= ns ? 1 : 0;
+    int32_t total;
+    const int32_t before = block_excl_scan<NT>(keep, wt, total);
     if (keep) out[pos + before] = m;
-    pos += __builtin_popcountll(bal);
+    pos += total;
   }
-  for (int32_t i = pos + lane; i < io.M; i += 64) out[i] = -1;
+  for (int32_t i = pos + tid; i < io.M; i += NT) out[i] = -1;
 }
 
 // ---------------------------------------------------------------- launchers
@@ -311,7 +316,7 @@ hipError_t launch_cs4a_map(const GeoTable& G, int S, int k, int32_t BH, int32_t 
   io.n_sink_tok = G.C[G.n_sink];
   io.rows = BH * io.G_k;
   if (io.rows == 0) return hipSuccess;
-  hipLaunchKernelGGL(cs4a_map_kernel, dim3(io.rows), dim3(64), 0, stream, io);
+  hipLaunchKernelGGL(cs4a_map_kernel, dim3(io.rows), dim3(kMapThreads), 0, stream, io);
   return hipGetLastError();
 }
 
