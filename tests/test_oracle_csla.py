@@ -1,0 +1,142 @@
+"""Pins of the CSLA oracle (token-wise sink-plus-local mask, 1-D block mask)
+against what the paper and the mathematics fix: hand-derived masks and block
+rows (tests/golden/csla_hand.json), exact-rational rounding, the paper's bound
+on the kept keys per query (N_sink + sum of w_h^2, reached by interior
+queries; 121 sink tokens on the first five Infinity scales), brute-force loops
+over query-key pairs for the block reduction, and closed forms (windows that
+cover every grid give dense attention)."""
+import json
+import os
+from fractions import Fraction
+
+import numpy as np
+
+import oracle as O
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+HAND = json.load(open(os.path.join(HERE, "golden", "csla_hand.json")))
+INF = [1, 2, 4, 6, 8, 12, 16, 20, 24, 32, 40, 48, 64]
+
+
+def hand_geom():
+    return O.Geometry(HAND["sides"], HAND["sides"], 1, 1)
+
+
+def test_aligned_centre_hand_values_and_rationals():
+    for c in HAND["centres"]:
+        assert O.aligned_centre(c["x"], c["n_k"], c["n_h"]) == c["expect"], c
+    for n_k in range(1, 30):
+        for n_h in range(1, n_k + 1):
+            for x in range(n_k):
+                t = Fraction(x * n_h, n_k)
+                want = int(t + Fraction(1, 2))  # t >= 0: floor(t + 1/2) rounds halves up
+                assert O.aligned_centre(x, n_k, n_h) == want
+    # same scale: the centre is the query itself
+    assert all(O.aligned_centre(x, 64, 64) == x for x in range(64))
+
+
+def test_token_mask_hand_rows():
+    g = hand_geom()
+    m = O.csla_token_mask(g, HAND["k"], HAND["n_sink_scales"], HAND["windows"])
+    assert m.shape == (16, 21)
+    for c in HAND["token_rows"]:
+        q = c["x"] * 4 + c["y"]
+        assert np.flatnonzero(m[q]).tolist() == c["expect"], c
+
+
+def test_token_mask_hand_rows_non_square():
+    c = HAND["nonsquare"]
+    g = O.Geometry(c["h"], c["w"], 1, 0)
+    m = O.csla_token_mask(g, c["k"], c["n_sink_scales"], c["windows"])
+    for row in c["token_rows"]:
+        q = row["x"] * c["w"][-1] + row["y"]
+        assert np.flatnonzero(m[q]).tolist() == row["expect"], row
+
+
+def test_block_rows_hand_values():
+    g = hand_geom()
+    m = O.csla_token_mask(g, HAND["k"], HAND["n_sink_scales"], HAND["windows"])
+    assert O.csla_block_rows(m, HAND["block_B"]) == HAND["block_rows"]
+
+
+def test_block_rows_brute_force_over_pairs():
+    r = np.random.default_rng(11)
+    for trial in range(6):
+        n_q, n_kv, B = int(r.integers(1, 40)), int(r.integers(1, 60)), int(r.integers(1, 9))
+        m = r.random((n_q, n_kv)) < 0.05
+        kept = set()
+        for i in range(n_q):
+            for j in range(n_kv):
+                if m[i, j]:
+                    kept.add((i // B, j // B))
+        rows = O.csla_block_rows(m, B)
+        assert len(rows) == -(-n_q // B)
+        assert [(u, v) for u, row in enumerate(rows) for v in row] == sorted(kept)
+        # B = 1 gives the token mask itself
+        assert O.csla_block_rows(m, 1) == [np.flatnonzero(m[i]).tolist() for i in range(n_q)]
+        # the block mask covers the token mask
+        bm = O.csla_block_mask(rows, n_q, n_kv, B)
+        assert (bm | ~m).all()
+
+
+def test_paper_sink_size_and_default_windows():
+    g = O.Geometry(INF, INF, 8, 4)
+    assert g.C(5) == 121 and g.C(13) == 10521 and g.N(13) == 4096
+    assert O.default_windows(13) == [0] * 10 + [3, 5, 7]
+    assert O.default_windows(2) == [5, 7]
+
+
+def test_kept_keys_per_query_meet_the_papers_bound():
+    # the complexity appendix bounds the keys of a query by N_sink + sum of w_h^2;
+    # a query whose windows all lie inside their grids keeps exactly that many
+    g = O.Geometry(INF, INF, 8, 4)
+    k, windows = 13, O.default_windows(13)
+    m = O.csla_token_mask(g, k, 5, windows)
+    cnt = m.sum(axis=1)
+    bound = 121 + 9 + 25 + 49
+    assert cnt.max() == bound
+    x, y = 32, 20  # centres (20, 13) on scale 11 and (24, 15) on scale 12: interior everywhere
+    assert cnt[x * 64 + y] == bound
+    # own token, and nothing outside sinks and the three windowed scales
+    q = np.arange(4096)
+    assert m[q, g.C(12) + q].all()
+    assert not m[:, 121:g.C(10)].any()
+
+
+def test_windows_are_monotone_and_zero_windows_leave_sinks():
+    g = O.Geometry([1, 2, 3, 5, 8], [1, 3, 4, 6, 9], 2, 1)
+    small = O.csla_token_mask(g, 5, 2, [0, 0, 1, 3, 3])
+    big = O.csla_token_mask(g, 5, 2, [0, 0, 3, 5, 7])
+    assert (big | ~small).all() and big.sum() > small.sum()
+    sinks = O.csla_token_mask(g, 5, 2, [0] * 5)
+    assert (sinks[:, :g.C(2)]).all() and not sinks[:, g.C(2):].any()
+    # a window on a sink scale does not shrink the sink: the masks are ORed
+    assert O.csla_token_mask(g, 5, 2, [1, 1, 0, 0, 0])[:, :g.C(2)].all()
+    rows = O.csla_block_rows(sinks, 4)
+    assert all(row == list(range(-(-g.C(2) // 4))) for row in rows)
+
+
+def test_covering_windows_give_dense_attention():
+    g = O.Geometry([1, 2, 3, 5], [1, 2, 4, 6], 2, 1)
+    k = 4
+    m = O.csla_token_mask(g, k, 0, [13] * k)  # radius 6 covers every grid
+    assert m.all()
+    r = np.random.default_rng(12)
+    q, kk, v = r.standard_normal((30, 8)), r.standard_normal((g.C(k), 8)), r.standard_normal((g.C(k), 8))
+    rows = O.csla_block_rows(m, 8)
+    o, lse = O.csla_attention(q, kk, v, rows, 8, 0.3)
+    od, ld = O.dense_attention(q, kk, v, 0.3)
+    assert np.allclose(o, od, atol=1e-12) and np.allclose(lse, ld, atol=1e-12)
+
+
+def test_block_attention_equals_masked_attention_of_the_block_mask():
+    g = O.Geometry(INF[:6], INF[:6], 8, 4)
+    k = 6
+    m = O.csla_token_mask(g, k, 3, O.default_windows(k))
+    for B in (4, 16, 32):
+        rows = O.csla_block_rows(m, B)
+        r = np.random.default_rng(B)
+        q, kk, v = r.standard_normal((g.N(k), 6)), r.standard_normal((g.C(k), 6)), r.standard_normal((g.C(k), 6))
+        o, lse = O.csla_attention(q, kk, v, rows, B, 0.5)
+        om, lm = O.masked_attention(q, kk, v, O.csla_block_mask(rows, g.N(k), g.C(k), B), 0.5)
+        assert np.allclose(o, om, atol=1e-12) and np.allclose(lse, lm, atol=1e-12)
