@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--sweep", action="store_true",
                     help="instead of the step line: one JSON line per setting of the wider-head, 2048x2048 and "
                          "sparsity-sweep workloads (per-layer times, TFLOP/s, density, speedup)")
+    ap.add_argument("--csla", action="store_true",
+                    help="instead of the step line: the CSLA block-path settings only")
     return ap.parse_args()
 
 
@@ -345,6 +347,75 @@ def sweep_cs4a(dev):
         del path
 
 
+# Block form of Cross-Scale Local Sparse Attention at the last Infinity scale with
+# 24 heads (4096 queries against 10521 keys, d = 128, batch 1): sink scales and
+# window sizes on the last three scales, 1-D blocks on both axes.
+CSLA_SWEEP = ([dict(block=64, n_sink=5, sizes=(3, 5, 7)), dict(block=128, n_sink=5, sizes=(3, 5, 7))]
+              + [dict(block=128, n_sink=5, sizes=z) for z in ((1, 3, 5), (3, 3, 3), (5, 5, 5), (5, 7, 9),
+                                                             (7, 7, 7), (7, 9, 11))]
+              + [dict(block=128, n_sink=n, sizes=(3, 5, 7)) for n in (6, 7, 8, 0)])
+
+
+def sweep_csla(dev, only=None):
+    """CSLA block path: block-row build and attention times, kept density and the
+    attention's algorithmic TFLOP/s (4 d * kept query-key pairs), against our
+    dense kernel at the same shape."""
+    import torch
+
+    from paper_2602_04361_amd import sparvar as sv
+    from paper_2602_04361_amd.synth import make_qkv
+
+    B, H, d, k = 1, 24, 128, 13
+    n0 = sum(x * x for x in SIDES[:k - 1])
+    n_q, n_kv = SIDES[k - 1] ** 2, n0 + SIDES[k - 1] ** 2
+    sets = []
+    for s in range(2):
+        q, kk, v = make_qkv(SIDES, SIDES, B, H, d, CFG["n_freq"], 5, seed=100 + s, bf16=True)
+        sets.append((torch.from_numpy(q[:, :, n0:n_kv]).to(dev).to(torch.bfloat16),
+                     torch.from_numpy(kk).to(dev).to(torch.bfloat16), torch.from_numpy(v).to(dev).to(torch.bfloat16)))
+    o = torch.empty(B, H, n_q, d, dtype=torch.bfloat16, device=dev)
+    stream = torch.cuda.current_stream()
+    scale = 1.0 / math.sqrt(d)
+
+    def timed(fn, n=20):
+        for i in range(3):
+            fn(i)
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        for i in range(n):
+            evs[i][0].record(stream)
+            fn(i)
+            evs[i][1].record(stream)
+        torch.cuda.synchronize()
+        return float(np.median([a.elapsed_time(b) for a, b in evs]))
+
+    t_dense = timed(lambda i: sv.sparvar_dense_attn_fwd(*sets[i % 2], o, None, softmax_scale=scale))
+    dense_flops = 4.0 * d * B * H * n_q * n_kv
+    for st in CSLA_SWEEP if only is None else only:
+        g = sv.Geometry(SIDES, SIDES, CFG["b"], st["n_sink"])
+        blk = st["block"]
+        wins = [0] * (k - len(st["sizes"])) + list(st["sizes"])
+        M = sv.sparvar_csla_row_stride(g, k, blk)
+        rows = torch.empty(-(-n_q // blk), M, dtype=torch.int32, device=dev)
+        t_rows = timed(lambda i: sv.sparvar_csla_block_rows(g, k, wins, blk, rows))
+        t_attn = timed(lambda i: sv.sparvar_csla_attn_fwd(g, k, blk, *sets[i % 2], o, rows, softmax_scale=scale))
+        r = rows.cpu().numpy()
+        pairs = 0
+        for u in range(r.shape[0]):
+            ids = r[u][r[u] >= 0]
+            nq = min(blk, n_q - u * blk)
+            pairs += nq * int(sum(min(blk, n_kv - v * blk) for v in ids))
+        flops = 4.0 * d * B * H * pairs
+        print(json.dumps({"sweep": f"csla_b{blk}_sink{st['n_sink']}_w{'-'.join(map(str, st['sizes']))}",
+                          "B": B, "H": H, "n_q": n_q, "n_kv": n_kv, "block": blk, "n_sink_scales": st["n_sink"],
+                          "windows_last3": list(st["sizes"]), "rows_ms": t_rows, "attn_ms": t_attn,
+                          "density": pairs / (n_q * n_kv), "sparsity": 1.0 - pairs / (n_q * n_kv),
+                          "gflop": flops / 1e9, "tflops": flops / t_attn / 1e9,
+                          "frac_bf16_peak": flops / t_attn / 1e9 / PEAK_BF16_TFLOPS,
+                          "dense_ms": t_dense, "dense_tflops": dense_flops / t_dense / 1e9,
+                          "speedup_vs_own_dense": t_dense / t_attn}), flush=True)
+
+
 # ---------------------------------------------------------------- main
 def main():
     args = parse()
@@ -366,6 +437,10 @@ def main():
     if args.sweep:
         sweep(args, dev)
         sweep_cs4a(dev)
+        sweep_csla(dev)
+        return
+    if args.csla:
+        sweep_csla(dev)
         return
     B, H, d = CFG["B"], CFG["H"], CFG["d"]
     BH = B * H

@@ -299,6 +299,52 @@ int sparvar_block_sparse_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_
                                   const int32_t* col_idx, const int32_t* schedule,
                                   hipStream_t stream);
 
+/*
+ * Cross-Scale Local Sparse Attention in the paper's block form (Sec. 3.3:
+ * Cross-Scale Local Mapping, sink mask, Eq. block_mask), with 1-D blocks of
+ * `block` contiguous tokens on both axes: query block u holds queries
+ * [u*block, min((u+1)*block, N_k)) of scale k, key block v holds cache tokens
+ * [v*block, min((v+1)*block, N_<=k)). block is 32, 64, 128 or 256;
+ * ceil(N_<=k / block) <= 2048.
+ *
+ * Row stride of the block rows: ceil(N_<=k / block). Host-only; < 0 on error.
+ */
+int32_t sparvar_csla_row_stride(const sparvar_geometry_t* g, int32_t k, int32_t block);
+
+/*
+ * Block rows of scale k (1 <= k <= num_scales). A query (x, y) of scale k is
+ * aligned to historical scale h at (round(x h_h / h_k), round(y w_h / w_k)),
+ * halves rounded up and not clipped, and keeps the keys (x', y') of scale h
+ * with max(|cx - x'|, |cy - y'|) <= windows[h-1] / 2 (integer division; a
+ * window of 0 keeps no key of that scale); every token of scales
+ * 1..num_sink_scales is kept as well. Row u lists, ascending, the key blocks
+ * holding at least one kept (query of u, key) pair, then -1 up to the stride.
+ * Head independent: compute once per (geometry, k, windows, block).
+ *   windows: host int32 [k], window sizes w_h >= 0 (read during the call).
+ *   rows: int32 [G_k, M], G_k = ceil(N_k / block),
+ *   M >= sparvar_csla_row_stride(g, k, block).
+ */
+int sparvar_csla_block_rows(const sparvar_geometry_t* g, int32_t k, const int32_t* windows,
+                            int32_t block, int32_t* rows, int32_t M, hipStream_t stream);
+
+/*
+ * Block-sparse attention over the rows of sparvar_csla_block_rows: every
+ * query of block u of (b,h) attends, with one softmax, to every key of the
+ * key blocks of row u (shared by all (b,h)), up to its first id outside
+ * [0, ceil(N_<=k / block)). A row with no valid block yields o = 0 and
+ * lse = -inf. bf16 only.
+ *   q_k: [B,H,N_k,d] (plane stride q_bh_stride); k_lek, v_lek: [B,H,N_<=k,d]
+ *   (plane stride kv_bh_stride); o: [B,H,N_k,d] contiguous; lse (nullable):
+ *   [B,H,N_k] fp32; rows: int32 [G_k, M]. Ids of a row must be strictly
+ *   ascending before the first invalid one; otherwise values are unspecified
+ *   (never an access outside the inputs and outputs).
+ */
+int sparvar_csla_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t block, int32_t B,
+                          int32_t H, int32_t d, sparvar_dtype_t dtype, const void* q_k,
+                          int64_t q_bh_stride, const void* k_lek, const void* v_lek,
+                          int64_t kv_bh_stride, void* o, float* lse, float softmax_scale,
+                          const int32_t* rows, int32_t M, hipStream_t stream);
+
 /* Static description of a status code. */
 const char* sparvar_status_string(int status);
 /* Message of the last failed call on this thread ("" if none). */

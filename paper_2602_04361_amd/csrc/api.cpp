@@ -436,6 +436,84 @@ int sparvar_cs4a_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t C, int
   return hip_status(launch_token_attn(a, stream), "token attention launch");
 }
 
+namespace {
+int check_csla(const GeoTable& T, int32_t k, int32_t block) {
+  if (k < 1 || k > T.L) return fail(SPARVAR_ERR_INVALID, "scale %d outside [1, %d]", k, T.L);
+  if (block != 32 && block != 64 && block != 128 && block != 256)
+    return fail(SPARVAR_ERR_UNSUPPORTED, "block size %d is not 32, 64, 128 or 256", block);
+  if ((T.C[k] + (int64_t)block - 1) / block > kCslaMaxBlocks)
+    return fail(SPARVAR_ERR_UNSUPPORTED, "%d cache tokens make more than %d blocks of %d", T.C[k], kCslaMaxBlocks,
+                block);
+  return SPARVAR_OK;
+}
+}  // namespace
+
+int32_t sparvar_csla_row_stride(const sparvar_geometry_t* g, int32_t k, int32_t block) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if ((st = check_csla(T, k, block))) return st;
+  ok();
+  return (T.C[k] + block - 1) / block;
+}
+
+int sparvar_csla_block_rows(const sparvar_geometry_t* g, int32_t k, const int32_t* windows, int32_t block,
+                            int32_t* rows, int32_t M, hipStream_t stream) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if ((st = check_csla(T, k, block))) return st;
+  if (!windows || !rows) return fail(SPARVAR_ERR_INVALID, "windows and rows are required");
+  for (int h = 0; h < k; ++h)
+    if (windows[h] < 0 || windows[h] > (1 << 20)) return fail(SPARVAR_ERR_INVALID, "window %d of scale %d", windows[h], h + 1);
+  const int32_t need = (T.C[k] + block - 1) / block;
+  if (M < need) return fail(SPARVAR_ERR_CAPACITY, "row stride %d < %d", M, need);
+  const int64_t Gk = ((int64_t)T.h[k - 1] * T.w[k - 1] + block - 1) / block;
+  if (Gk * M >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "block rows too large");
+  return hip_status(launch_csla_rows(T, k, windows, block, rows, M, stream), "CSLA block rows launch");
+}
+
+int sparvar_csla_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t block, int32_t B, int32_t H, int32_t d,
+                          sparvar_dtype_t dtype, const void* q_k, int64_t q_bh_stride, const void* k_lek,
+                          const void* v_lek, int64_t kv_bh_stride, void* o, float* lse, float softmax_scale,
+                          const int32_t* rows, int32_t M, hipStream_t stream) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if ((st = check_csla(T, k, block))) return st;
+  if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
+  if ((st = check_dtype_d(dtype, d))) return st;
+  if (dtype != SPARVAR_BF16) return fail(SPARVAR_ERR_UNSUPPORTED, "the CSLA block path takes bf16 inputs");
+  if (!rows || M < 1) return fail(SPARVAR_ERR_INVALID, "rows and a row stride >= 1 are required");
+  if (!(std::isfinite(softmax_scale))) return fail(SPARVAR_ERR_INVALID, "softmax_scale is not finite");
+  const int32_t Nk = T.h[k - 1] * T.w[k - 1];
+  if ((int64_t)B * H * Nk >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "B*H*N_k too large");
+  if ((st = check_plane(q_k, q_bh_stride, Nk, d, 2, "q_k"))) return st;
+  if ((st = check_plane(k_lek, kv_bh_stride, T.C[k], d, 2, "k_lek"))) return st;
+  if ((st = check_plane(v_lek, kv_bh_stride, T.C[k], d, 2, "v_lek"))) return st;
+  if ((st = check_plane(o, (int64_t)Nk * d, Nk, d, 2, "o"))) return st;
+  const int64_t Gk = (Nk + block - 1) / block;
+  if (Gk * M >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "block rows too large");
+  BlockRowAttnArgs a;
+  a.BH = B * H;
+  a.n_q = Nk;
+  a.n_kv = T.C[k];
+  a.d = d;
+  a.block = block;
+  a.M = M;
+  a.q = q_k;
+  a.k = k_lek;
+  a.v = v_lek;
+  a.o = o;
+  a.lse = lse;
+  a.q_bh_stride = q_bh_stride;
+  a.kv_bh_stride = kv_bh_stride;
+  a.softmax_scale = softmax_scale;
+  a.block_rows = rows;
+  a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
+  return hip_status(launch_block_row_attn(a, stream), "CSLA attention launch");
+}
+
 int64_t sparvar_local_blocks_capacity(const sparvar_geometry_t* g, int32_t k, int32_t radius,
                                       int32_t prev_dilation) {
   GeoTable T;

@@ -146,6 +146,88 @@ struct TokenSrc {
   }
 };
 
+// Listed 1-D key blocks of B contiguous tokens: consecutive ids are merged into
+// one run of the cache, cut into chunks of at most KC keys. ids is the row's
+// valid block ids (ascending) staged in LDS.
+// The walk ends at the first id outside [0, nkb).
+template <int KC>
+struct RunCursor {
+  const int32_t* ids;
+  int32_t pos, len, B, n_kv, nkb, run_base, run_left;
+  __device__ __forceinline__ bool next(Chunk& c) {
+    if (run_left == 0) {
+      if (pos >= len) return false;
+      int32_t v = __builtin_amdgcn_readfirstlane(ids[pos]);
+      if ((uint32_t)v >= (uint32_t)nkb) {
+        pos = len;
+        return false;
+      }
+      ++pos;
+      run_base = v * B;
+      while (pos < len && __builtin_amdgcn_readfirstlane(ids[pos]) == v + 1) {
+        ++v;
+        ++pos;
+      }
+      const int32_t end = v * B + B;
+      run_left = (end < n_kv ? end : n_kv) - run_base;
+    }
+    const int32_t cnt = run_left < KC ? run_left : KC;
+    c = run_chunk(run_base, cnt);
+    run_base += cnt;
+    run_left -= cnt;
+    return true;
+  }
+};
+
+// 1-D query blocks of C = 32 NW contiguous queries, each with a row of 1-D key
+// blocks of C tokens (the CSLA block mask). Row g of rows, shared by every
+// (b, h), lists ascending ids in [0, ceil(n_kv / C)) followed by padding (any id
+// outside that range), at a fixed stride M; entries past kCslaMaxBlocks are not
+// read (a row holds at most ceil(n_kv / C) <= kCslaMaxBlocks valid ids).
+template <int KC>
+struct BlockRowSrc {
+  static constexpr bool kSparse = false;
+  static constexpr bool kGrouped = false;
+  static constexpr bool kTokens = false;
+  static constexpr bool kRuns = true;
+  const int32_t* rows;
+  int32_t M, C, n_q, n_kv, n_blocks;
+  template <int NT>
+  static constexpr int table_bytes() { return 4 * kCslaMaxBlocks; }
+  __device__ __forceinline__ int tile_of(int) const { return 0; }
+  __device__ __forceinline__ QuerySet queries(int32_t item, int wave) const {
+    QuerySet s;
+    s.bh = item / n_blocks;
+    const int32_t g = item - s.bh * n_blocks;
+    s.qbase = g * C;
+    s.qnc = 1 << 30;  // contiguous rows
+    s.qstride = 0;
+    s.q0 = wave * kQPerWave;
+    s.q1 = (n_q - g * C < C) ? n_q - g * C : C;
+    return s;
+  }
+  // Stages the row in LDS, by the whole workgroup.
+  template <int NT>
+  __device__ __forceinline__ RunCursor<KC> run_cursor(int32_t item, char* lds) const {
+    const int32_t g = item % n_blocks;
+    const int32_t* row = rows + (int64_t)g * M;
+    int32_t* ids = reinterpret_cast<int32_t*>(lds);
+    const int32_t lim = M < kCslaMaxBlocks ? M : kCslaMaxBlocks;
+    for (int32_t i = threadIdx.x; i < lim; i += NT) ids[i] = row[i];
+    __syncthreads();
+    RunCursor<KC> c;
+    c.ids = ids;
+    c.pos = 0;
+    c.len = lim;
+    c.B = C;
+    c.n_kv = n_kv;
+    c.nkb = (n_kv + C - 1) / C;
+    c.run_base = 0;
+    c.run_left = 0;
+    return c;
+  }
+};
+
 // Walks the kept blocks of one CSR row as chunks of at most KC keys.
 // Consecutive blocks whose tokens are contiguous in the cache (whole small
 // scales such as the sink scales) are merged into one run and cut at KC;
@@ -708,6 +790,12 @@ __device__ __forceinline__ char* stage_ptr(char* s0, char* s1, char* s2, char* s
   else return s3;
 }
 
+// Sources with a kRuns member walk listed 1-D key blocks (BlockRowSrc).
+template <class Src, class = void>
+constexpr bool kRunsOf = false;
+template <class Src>
+constexpr bool kRunsOf<Src, std::void_t<decltype(Src::kRuns)>> = Src::kRuns;
+
 // ---------------------------------------------------------------- bf16 kernel
 template <int D, int NW, int KC, int NS, class Src>
 __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) {
@@ -808,6 +896,8 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
   auto cur = [&]() {
     if constexpr (Src::kSparse) {
       return src.template table_cursor<NT>(item, tsmem);
+    } else if constexpr (kRunsOf<Src>) {
+      return src.template run_cursor<NT>(item, tsmem);
     } else if constexpr (Src::kTokens) {
       return src.template token_cursor<NT>(item, tsmem);
     } else {
@@ -1280,6 +1370,38 @@ hipError_t launch_token_attn(const TokenAttnArgs& a, hipStream_t stream) {
   if (a.d == DD && nw == NN) return launch_bf16<DD, NN, KK, 2>(io, make(TokenSrc<KK>{}), stream);
   SV_TOKEN_SHAPES(SV_TOK)
 #undef SV_TOK
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_block_row_attn(const BlockRowAttnArgs& a, hipStream_t stream) {
+  const int nw = a.block / kQPerWave;
+  AttnIO io;
+  io.q = a.q;
+  io.k = a.k;
+  io.v = a.v;
+  io.o = a.o;
+  io.lse = a.lse;
+  io.q_bh_stride = a.q_bh_stride;
+  io.kv_bh_stride = a.kv_bh_stride;
+  io.o_rows = a.n_q;
+  const int32_t n_blocks = (a.n_q + a.block - 1) / a.block;
+  io.n_items = a.BH * n_blocks;
+  io.swizzle = a.swizzle;
+  io.scale_log2 = a.softmax_scale * kLog2e;
+  auto make = [&](auto proto) {
+    auto s = proto;
+    s.rows = a.block_rows;
+    s.M = a.M;
+    s.C = a.block;
+    s.n_q = a.n_q;
+    s.n_kv = a.n_kv;
+    s.n_blocks = n_blocks;
+    return s;
+  };
+#define SV_BLK(DD, NN, KK) \
+  if (a.d == DD && nw == NN) return launch_bf16<DD, NN, KK, 2>(io, make(BlockRowSrc<KK>{}), stream);
+  SV_TOKEN_SHAPES(SV_BLK)
+#undef SV_BLK
   return hipErrorInvalidValue;
 }
 

@@ -92,7 +92,28 @@ struct TokenAttnArgs {
   int swizzle;
 };
 
+// 1-D key blocks of the CSLA block mask: row g (shared by every (b, h)) of
+// block_rows lists, ascending, the key blocks [v B, min(v B + B, n_kv)) of
+// query block g (queries [g B, min(g B + B, n_q))), then padding.
+struct BlockRowAttnArgs {
+  int32_t BH, n_q, n_kv, d, block, M;
+  const void *q, *k, *v;
+  void* o;
+  float* lse;
+  int64_t q_bh_stride, kv_bh_stride;
+  float softmax_scale;
+  const int32_t* block_rows;
+  int swizzle;
+};
+
+// Key blocks a 1-D block row may list (LDS bitmask of the row builder, LDS id
+// table of the attention kernel).
+constexpr int32_t kCslaMaxBlocks = 2048;
+
 hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream);
+hipError_t launch_block_row_attn(const BlockRowAttnArgs& a, hipStream_t stream);
+hipError_t launch_csla_rows(const GeoTable& G, int k, const int32_t* windows, int32_t B, int32_t* rows, int32_t M,
+                            hipStream_t stream);
 hipError_t launch_token_attn(const TokenAttnArgs& a, hipStream_t stream);
 hipError_t launch_cs4a_colsum(const Cs4aColsumArgs& a, hipStream_t stream);
 hipError_t launch_cs4a_topk(const float* in, int32_t rows, int32_t n, int32_t K, int32_t* out, hipStream_t stream);

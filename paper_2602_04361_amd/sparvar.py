@@ -28,6 +28,9 @@ EXPORTS = [
     "sparvar_cs4a_row_stride",
     "sparvar_cs4a_map_tokens",
     "sparvar_cs4a_attn_fwd",
+    "sparvar_csla_row_stride",
+    "sparvar_csla_block_rows",
+    "sparvar_csla_attn_fwd",
     "sparvar_local_blocks_capacity",
     "sparvar_local_blocks",
     "sparvar_map_index_capacity",
@@ -85,6 +88,10 @@ def load_library(path: str = LIB_PATH):
                                                     f32, vp, vp]),
         "sparvar_cs4a_select_tokens": (ctypes.c_int, [vp, i32, i32, i32, vp, vp]),
         "sparvar_cs4a_row_stride": (i32, [G, i32]),
+        "sparvar_csla_row_stride": (i32, [G, i32, i32]),
+        "sparvar_csla_block_rows": (ctypes.c_int, [G, i32, vp, i32, vp, i32, vp]),
+        "sparvar_csla_attn_fwd": (ctypes.c_int, [G, i32, i32, i32, i32, i32, ctypes.c_int, vp, i64, vp, vp, i64, vp,
+                                                 vp, ctypes.c_float, vp, i32, vp]),
         "sparvar_cs4a_map_tokens": (ctypes.c_int, [G, i32, i32, i32, i32, i32, i32, vp, vp, i32, vp]),
         "sparvar_cs4a_attn_fwd": (ctypes.c_int, [G, i32, i32, i32, i32, i32, ctypes.c_int, vp, i64, vp, vp, i64, vp,
                                                  vp, f32, vp, i32, i32, vp, i32, vp]),
@@ -266,6 +273,36 @@ def sparvar_cs4a_attn_fwd(geom, k, C, q_k, k_lek, v_lek, o, tokens, M, lse=None,
     _check(lib.sparvar_cs4a_attn_fwd(geom.ref, k, C, B, H, d, _dtype_code(q_k), _ptr(q_k), _plane_stride(q_k, "q_k"),
                                      _ptr(k_lek), _ptr(v_lek), _plane_stride(k_lek, "k_lek"), _ptr(o), _ptr(lse),
                                      _scale(softmax_scale, d), _ptr(tokens), M, mode, _ptr(base), base_scale,
+                                     _stream(stream)))
+    return o
+
+
+def sparvar_csla_row_stride(geom, k, block):
+    m = load_library().sparvar_csla_row_stride(geom.ref, k, block)
+    if m < 0:
+        _check(int(m))
+    return int(m)
+
+
+def sparvar_csla_block_rows(geom, k, windows, block, rows, stream=None):
+    """CSLA key-block rows of every 1-D query block of scale k (windows: one size per scale 1..k); see sparvar.h."""
+    win = (ctypes.c_int32 * max(len(windows), 1))(*[int(w) for w in windows])
+    if len(windows) != k:
+        raise SparvarError(ERR_INVALID, "one window size per scale 1..k is required")
+    _check(load_library().sparvar_csla_block_rows(geom.ref, k, ctypes.cast(win, ctypes.c_void_p), block, _ptr(rows),
+                                                  rows.shape[-1], _stream(stream)))
+    return rows
+
+
+def sparvar_csla_attn_fwd(geom, k, block, q_k, k_lek, v_lek, o, rows, lse=None, softmax_scale=None, stream=None):
+    """Block-sparse attention of scale k over CSLA block rows (shared by every head)."""
+    lib = load_library()
+    B, H, _, d = q_k.shape
+    if _plane_stride(v_lek, "v_lek") != _plane_stride(k_lek, "k_lek"):
+        raise SparvarError(ERR_INVALID, "k_lek and v_lek must share one plane stride")
+    _check(lib.sparvar_csla_attn_fwd(geom.ref, k, block, B, H, d, _dtype_code(q_k), _ptr(q_k),
+                                     _plane_stride(q_k, "q_k"), _ptr(k_lek), _ptr(v_lek), _plane_stride(k_lek, "k_lek"),
+                                     _ptr(o), _ptr(lse), _scale(softmax_scale, d), _ptr(rows), rows.shape[-1],
                                      _stream(stream)))
     return o
 

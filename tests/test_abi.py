@@ -147,3 +147,39 @@ def test_decision_step_validation_before_launch():
     assert call(args(v=None)) == sv.ERR_INVALID
     assert call(args(kvs=100)) == sv.ERR_INVALID       # plane stride shorter than the plane
     assert call(args(scale=float("inf"))) == sv.ERR_INVALID
+
+
+def test_csla_validation_before_launch():
+    lib = sv.load_library()
+    vp = ctypes.c_void_p
+    fake = vp(1 << 20)
+    g = sv.Geometry(INF, INF, 8, 5)
+    # row stride = key blocks of the cache at step k
+    assert sv.sparvar_csla_row_stride(g, 13, 128) == 83 and sv.sparvar_csla_row_stride(g, 13, 64) == 165
+    assert sv.sparvar_csla_row_stride(g, 11, 32) == -(-4121 // 32)
+    assert lib.sparvar_csla_row_stride(g.ref, 13, 48) == sv.ERR_UNSUPPORTED   # block size
+    assert lib.sparvar_csla_row_stride(g.ref, 14, 64) == sv.ERR_INVALID       # scale out of range
+    big = sv.Geometry([256, 300], [256, 300], 8, 1)                            # more than 2048 key blocks of 32
+    assert lib.sparvar_csla_row_stride(big.ref, 2, 32) == sv.ERR_UNSUPPORTED
+    win = (ctypes.c_int32 * 13)(*([0] * 10 + [3, 5, 7]))
+    neg = (ctypes.c_int32 * 13)(*([0] * 12 + [-1]))
+    wp = ctypes.cast(win, vp)
+    assert lib.sparvar_csla_block_rows(g.ref, 13, wp, 128, fake, 82, None) == sv.ERR_CAPACITY
+    assert lib.sparvar_csla_block_rows(g.ref, 13, ctypes.cast(neg, vp), 128, fake, 83, None) == sv.ERR_INVALID
+    assert lib.sparvar_csla_block_rows(g.ref, 13, None, 128, fake, 83, None) == sv.ERR_INVALID
+    assert lib.sparvar_csla_block_rows(g.ref, 13, wp, 128, None, 83, None) == sv.ERR_INVALID
+
+    def attn(**kw):
+        a = dict(k=13, block=128, B=1, H=24, d=128, dt=sv.BF16, q=fake, qs=4096 * 128, kk=fake, v=fake,
+                 kvs=10521 * 128, o=fake, scale=0.1, rows=fake, M=83)
+        a.update(kw)
+        return lib.sparvar_csla_attn_fwd(g.ref, a["k"], a["block"], a["B"], a["H"], a["d"], a["dt"], a["q"], a["qs"],
+                                         a["kk"], a["v"], a["kvs"], a["o"], None, a["scale"], a["rows"], a["M"], None)
+    assert attn(block=96) == sv.ERR_UNSUPPORTED
+    assert attn(dt=sv.F32) == sv.ERR_UNSUPPORTED
+    assert attn(d=96) == sv.ERR_UNSUPPORTED
+    assert attn(rows=None) == sv.ERR_INVALID
+    assert attn(M=0) == sv.ERR_INVALID
+    assert attn(kvs=100) == sv.ERR_INVALID
+    assert attn(scale=float("nan")) == sv.ERR_INVALID
+    assert attn(k=0) == sv.ERR_INVALID
