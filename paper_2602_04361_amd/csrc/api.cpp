@@ -189,6 +189,7 @@ int sparvar_dense_attn_fwd(int32_t B, int32_t H, int32_t n_q, int32_t n_kv, int3
   a.chunk = env_int("SPARVAR_DENSE_CHUNK", 64);
   a.stages = env_int("SPARVAR_DENSE_STAGES", 2);
   a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
+  a.num_cu = device_cus();
   return hip_status(launch_dense_attn(a, stream), "dense attention launch");
 }
 
@@ -510,6 +511,9 @@ int sparvar_csla_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t block,
   a.kv_bh_stride = kv_bh_stride;
   a.softmax_scale = softmax_scale;
   a.block_rows = rows;
+  // 32-key chunks in three stages fit three 4-wave workgroups per CU (d = 128)
+  a.chunk = env_int("SPARVAR_CSLA_CHUNK", 32);
+  a.stages = env_int("SPARVAR_CSLA_STAGES", 3);
   a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
   return hip_status(launch_block_row_attn(a, stream), "CSLA attention launch");
 }

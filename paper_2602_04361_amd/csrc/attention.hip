@@ -147,24 +147,30 @@ struct TokenSrc {
 };
 
 // Listed 1-D key blocks of B contiguous tokens: consecutive ids are merged into
-// one run of the cache, cut into chunks of at most KC keys. ids is the row's
-// valid block ids (ascending) staged in LDS.
+// one run of the cache, cut into chunks of at most KC keys. The first kRunTable
+// entries of the row are staged in LDS; later ones are read from global memory.
 // The walk ends at the first id outside [0, nkb).
+constexpr int kRunTable = 512;
+
 template <int KC>
 struct RunCursor {
-  const int32_t* ids;
+  const int32_t* ids;  // LDS
+  const int32_t* row;  // global
   int32_t pos, len, B, n_kv, nkb, run_base, run_left;
+  __device__ __forceinline__ int32_t id_at(int32_t p) const {
+    return __builtin_amdgcn_readfirstlane(p < kRunTable ? ids[p] : row[p]);
+  }
   __device__ __forceinline__ bool next(Chunk& c) {
     if (run_left == 0) {
       if (pos >= len) return false;
-      int32_t v = __builtin_amdgcn_readfirstlane(ids[pos]);
+      int32_t v = id_at(pos);
       if ((uint32_t)v >= (uint32_t)nkb) {
         pos = len;
         return false;
       }
       ++pos;
       run_base = v * B;
-      while (pos < len && __builtin_amdgcn_readfirstlane(ids[pos]) == v + 1) {
+      while (pos < len && id_at(pos) == v + 1) {
         ++v;
         ++pos;
       }
@@ -182,8 +188,7 @@ struct RunCursor {
 // 1-D query blocks of C = 32 NW contiguous queries, each with a row of 1-D key
 // blocks of C tokens (the CSLA block mask). Row g of rows, shared by every
 // (b, h), lists ascending ids in [0, ceil(n_kv / C)) followed by padding (any id
-// outside that range), at a fixed stride M; entries past kCslaMaxBlocks are not
-// read (a row holds at most ceil(n_kv / C) <= kCslaMaxBlocks valid ids).
+// outside that range), at a fixed stride M.
 template <int KC>
 struct BlockRowSrc {
   static constexpr bool kSparse = false;
@@ -193,7 +198,7 @@ struct BlockRowSrc {
   const int32_t* rows;
   int32_t M, C, n_q, n_kv, n_blocks;
   template <int NT>
-  static constexpr int table_bytes() { return 4 * kCslaMaxBlocks; }
+  static constexpr int table_bytes() { return 4 * kRunTable; }
   __device__ __forceinline__ int tile_of(int) const { return 0; }
   __device__ __forceinline__ QuerySet queries(int32_t item, int wave) const {
     QuerySet s;
@@ -206,19 +211,20 @@ struct BlockRowSrc {
     s.q1 = (n_q - g * C < C) ? n_q - g * C : C;
     return s;
   }
-  // Stages the row in LDS, by the whole workgroup.
+  // Stages the head of the row in LDS, by the whole workgroup.
   template <int NT>
   __device__ __forceinline__ RunCursor<KC> run_cursor(int32_t item, char* lds) const {
     const int32_t g = item % n_blocks;
     const int32_t* row = rows + (int64_t)g * M;
     int32_t* ids = reinterpret_cast<int32_t*>(lds);
-    const int32_t lim = M < kCslaMaxBlocks ? M : kCslaMaxBlocks;
+    const int32_t lim = M < kRunTable ? M : kRunTable;
     for (int32_t i = threadIdx.x; i < lim; i += NT) ids[i] = row[i];
     __syncthreads();
     RunCursor<KC> c;
     c.ids = ids;
+    c.row = row;
     c.pos = 0;
-    c.len = lim;
+    c.len = M;
     c.B = C;
     c.n_kv = n_kv;
     c.nkb = (n_kv + C - 1) / C;
@@ -1289,17 +1295,46 @@ void shape_for(int d, int nw, int want_kc, int want_ns, int* kc, int* ns) {
 
 }  // namespace
 
+namespace {
+// Workgroups that fit a CU at once for the two bf16 dense shapes compared below
+// (register-bound: about 240 VGPRs for 8 waves with 64-key chunks give one
+// workgroup; about 160 VGPRs for 4 waves with 32-key chunks (64 at d = 64) give
+// three).
+constexpr int kDenseWgsPerCu8 = 1;
+constexpr int kDenseWgsPerCu4 = 3;
+
+// Share of the launch's last round of workgroups that is busy: n workgroups over
+// cus * per_cu slots.
+double last_round_fill(int64_t n, int64_t cus, int per_cu) {
+  const int64_t slots = cus * per_cu;
+  const int64_t rounds = (n + slots - 1) / slots;
+  return rounds == 0 ? 1.0 : (double)n / (double)(rounds * slots);
+}
+}  // namespace
+
 hipError_t launch_dense_attn(const DenseAttnArgs& a, hipStream_t stream) {
   // Widest workgroup (most queries sharing each K/V chunk) that still gives every
-  // one of the 256 CUs a workgroup: 8 waves, else 4 waves, else 2 waves with
-  // 32-key chunks.
+  // CU a workgroup: 8 waves, else 4 waves, else 2 waves with 32-key chunks. In
+  // bf16, 4 waves with 32-key chunks (several workgroups per CU) replace 8 waves
+  // when they fill the CUs' slots more evenly.
   auto wgs = [&](int w) { return (int64_t)a.BH * ((a.n_q + 32 * w - 1) / (32 * w)); };
   int nw = a.waves;
   int want_kc = a.chunk;
   if (nw <= 0) {
-    if (wgs(8) >= 256) nw = 8;
-    else if (wgs(4) >= 256) nw = 4;
-    else {
+    const int64_t cus = a.num_cu > 0 ? a.num_cu : 256;
+    if (wgs(8) >= cus) {
+      nw = 8;
+      if (a.bf16 && a.stages == 2 && want_kc == 64) {
+        const double f8 = last_round_fill(wgs(8), cus, kDenseWgsPerCu8);
+        const double f4 = last_round_fill(wgs(4), cus, kDenseWgsPerCu4);
+        if (f4 > f8 + 0.05) {
+          nw = 4;
+          want_kc = a.d == 128 ? 32 : 64;
+        }
+      }
+    } else if (wgs(4) >= cus) {
+      nw = 4;
+    } else {
       nw = 2;
       want_kc = 32;
     }
@@ -1398,9 +1433,16 @@ hipError_t launch_block_row_attn(const BlockRowAttnArgs& a, hipStream_t stream) 
     s.n_blocks = n_blocks;
     return s;
   };
-#define SV_BLK(DD, NN, KK) \
-  if (a.d == DD && nw == NN) return launch_bf16<DD, NN, KK, 2>(io, make(BlockRowSrc<KK>{}), stream);
-  SV_TOKEN_SHAPES(SV_BLK)
+  int kc = a.chunk, ns = a.stages;
+  if (!(a.d == 128 && nw >= 2 && kc == 32 && (ns == 3 || ns == 4))) kc = 64, ns = 2;
+#define SV_BLK(DD, NN, KK, SS) \
+  if (a.d == DD && nw == NN && kc == KK && ns == SS) \
+    return launch_bf16<DD, NN, KK, SS>(io, make(BlockRowSrc<KK>{}), stream);
+#define SV_BLK2(DD, NN, KK) SV_BLK(DD, NN, KK, 2)
+  SV_TOKEN_SHAPES(SV_BLK2)
+  SV_BLK(128, 2, 32, 3) SV_BLK(128, 4, 32, 3) SV_BLK(128, 8, 32, 3)
+  SV_BLK(128, 2, 32, 4) SV_BLK(128, 4, 32, 4) SV_BLK(128, 8, 32, 4)
+#undef SV_BLK2
 #undef SV_BLK
   return hipErrorInvalidValue;
 }

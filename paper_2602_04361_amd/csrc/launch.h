@@ -20,6 +20,7 @@ struct DenseAttnArgs {
   int chunk;    // keys per chunk (32 or 64)
   int stages;   // LDS pipeline depth
   int swizzle;  // XCD-aware workgroup order
+  int num_cu;   // compute units of the device (automatic launch choices)
 };
 
 struct SparseAttnArgs {
@@ -103,11 +104,12 @@ struct BlockRowAttnArgs {
   int64_t q_bh_stride, kv_bh_stride;
   float softmax_scale;
   const int32_t* block_rows;
+  int chunk;   // keys per chunk: 64 (two stages), or 32 with 3 or 4 stages (d = 128, >= 2 waves)
+  int stages;
   int swizzle;
 };
 
-// Key blocks a 1-D block row may list (LDS bitmask of the row builder, LDS id
-// table of the attention kernel).
+// Key blocks a 1-D block row may list (LDS bitmask of the row builder).
 constexpr int32_t kCslaMaxBlocks = 2048;
 
 hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream);

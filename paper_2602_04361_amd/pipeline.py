@@ -168,3 +168,39 @@ class Cs4aPath:
         self.decision(Q_all, K_all, V_all)
         for k in self.steps:
             self.step(k, Q_all, K_all, V_all)
+
+
+class CslaPath:
+    """One layer of the paper-literal CSLA block path (Sec. 3.3) as C-ABI calls.
+
+    The block rows of each sparse scale depend only on the geometry, the window
+    sizes and the block size, so they are built once (rows()) and reused by every
+    layer and head; step(k) runs the block-sparse attention of scale k.
+    windows[k] lists one window size per scale 1..k (0: no local keys there).
+    """
+
+    def __init__(self, geom: sv.Geometry, steps, windows, block, B, H, d, device="cuda", softmax_scale=None):
+        self.g = geom
+        self.steps = [int(k) for k in steps]
+        self.windows = {int(k): [int(w) for w in windows[k]] for k in self.steps}
+        self.block, self.B, self.H, self.d = int(block), B, H, d
+        self.scale = float(torch.tensor(1.0 / math.sqrt(d), dtype=torch.float32)) if softmax_scale is None \
+            else float(softmax_scale)
+        self.info = {l: geom.scale_info(l) for l in range(1, len(geom.h) + 1)}
+        self.block_rows, self.out = {}, {}
+        for k in self.steps:
+            M = sv.sparvar_csla_row_stride(geom, k, self.block)
+            G_k = -(-self.info[k]["n_tokens"] // self.block)
+            self.block_rows[k] = torch.empty(G_k, M, dtype=torch.int32, device=device)
+            self.out[k] = torch.empty(B, H, self.info[k]["n_tokens"], d, dtype=torch.bfloat16, device=device)
+
+    def rows(self):
+        for k in self.steps:
+            sv.sparvar_csla_block_rows(self.g, k, self.windows[k], self.block, self.block_rows[k])
+
+    def step(self, k, Q_all, K_all, V_all):
+        i = self.info[k]
+        sv.sparvar_csla_attn_fwd(self.g, k, self.block, Q_all[:, :, i["token_offset"]:i["n_tokens_le"]],
+                                 K_all[:, :, :i["n_tokens_le"]], V_all[:, :, :i["n_tokens_le"]], self.out[k],
+                                 self.block_rows[k], softmax_scale=self.scale)
+        return self.out[k]

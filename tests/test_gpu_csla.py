@@ -129,3 +129,52 @@ def test_attention_empty_rows_give_zero_and_stop_at_first_invalid_id():
     got = o.float().cpu().numpy()[0, 0]
     ref, _ = O.csla_attention(q[0, 0, og.C(7):og.C(8)], kk[0, 0], v[0, 0], [[0, 3]] * n_rows, block, scale_of(d))
     assert_close(got, ref, "bf16", "rows cut at the first invalid id")
+
+
+@pytest.mark.parametrize("stages", [3, 4])
+def test_attention_chunks_of_32(monkeypatch, stages):
+    # the 32-key chunk shapes (d = 128, two to eight waves)
+    monkeypatch.setenv("SPARVAR_CSLA_CHUNK", "32")
+    monkeypatch.setenv("SPARVAR_CSLA_STAGES", str(stages))
+    for block in (64, 128, 256):
+        attn_case(INF_SIDES[:10], 5, 10, O.default_windows(10), block, 1, 2, 128, 56 + block)
+
+
+def test_rows_longer_than_the_lds_table():
+    # every scale a sink: each of the 200 query blocks of the 80x80 scale lists all
+    # 529 key blocks of 32, past the ids staged in LDS
+    h = INF_SIDES + [80]
+    k = 14
+    rows, want = check_rows(h, h, k, k, [0] * k, 32)
+    assert all(len(r) == 529 for r in want)
+    g = sv.Geometry(h, h, 8, k)
+    og = O.Geometry(h, h, 8, k)
+    q, kk, v = make_case(h, h, 1, 1, 128, 16, 4, 57, "bf16")
+    n0, n1 = og.C(k - 1), og.C(k)
+    Q, Kd, Vd = to_dev(q[:, :, n0:n1], "bf16"), to_dev(kk, "bf16"), to_dev(v, "bf16")
+    o = torch.empty_like(Q)
+    sv.sparvar_csla_attn_fwd(g, k, 32, Q, Kd, Vd, o, rows)
+    torch.cuda.synchronize()
+    ref, _ = O.dense_attention(q[0, 0, n0:n1], kk[0, 0], v[0, 0], scale_of(128))
+    assert_close(o.float().cpu().numpy()[0, 0], ref, "bf16", "every block kept")
+
+
+def test_pipeline_last_three_scales():
+    from paper_2602_04361_amd.pipeline import CslaPath
+
+    h, ns, block, d = INF_SIDES, 5, 128, 128
+    steps = [11, 12, 13]
+    note(f"[csla pipeline] steps={steps} block={block}")
+    g = sv.Geometry(h, h, 8, ns)
+    og = O.Geometry(h, h, 8, ns)
+    q, kk, v = make_case(h, h, 1, 2, d, 16, ns, 58, "bf16")
+    Qd, Kd, Vd = to_dev(q, "bf16"), to_dev(kk, "bf16"), to_dev(v, "bf16")
+    path = CslaPath(g, steps, {k: O.default_windows(k) for k in steps}, block, 1, 2, d)
+    path.rows()
+    outs = {k: path.step(k, Qd, Kd, Vd) for k in steps}
+    torch.cuda.synchronize()
+    for k in steps:
+        rows = O.csla_block_rows(O.csla_token_mask(og, k, ns, O.default_windows(k)), block)
+        ref, _ = O.csla_attention(q[0, 1, og.C(k - 1):og.C(k)], kk[0, 1, :og.C(k)], v[0, 1, :og.C(k)], rows, block,
+                                  scale_of(d))
+        assert_close(outs[k].float().cpu().numpy()[0, 1], ref, "bf16", f"step {k}")
