@@ -275,6 +275,25 @@ int sparvar_map_index(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t
                       hipStream_t stream);
 
 /*
+ * Index mapping for several target scales in one launch: for each i <
+ * n_steps (1 <= n_steps <= 8), the rows of scale ks[i] exactly as
+ * sparvar_map_index(g, S, ks[i], B, H, topk, topk_idx, NULL, NULL, radius,
+ * prev_dilation, row_ptrs[i], col_idxs[i], capacities[i], NULL, stream) writes
+ * them (local rows generated in the call, no schedule). The mapping of every
+ * later scale depends only on the selection at S, so all of them can be built
+ * right after the decision step.
+ *   ks, row_ptrs, col_idxs, capacities: host arrays of n_steps entries, read
+ *   during the call; row_ptrs[i], col_idxs[i] are device buffers sized as for
+ *   sparvar_map_index, capacities[i] >= sparvar_map_index_capacity(g, S,
+ *   ks[i], B, H, topk, radius, prev_dilation).
+ */
+int sparvar_map_index_steps(const sparvar_geometry_t* g, int32_t S, int32_t n_steps, const int32_t* ks,
+                            int32_t B, int32_t H, int32_t topk, const int32_t* topk_idx,
+                            int32_t radius, int32_t prev_dilation, int32_t* const* row_ptrs,
+                            int32_t* const* col_idxs, const int64_t* capacities,
+                            hipStream_t stream);
+
+/*
  * Block-sparse cross-scale attention at scale k (the sparse update
  * Delta O of Sec. 3.2 and the block-masked attention of Sec. 3.3, Eq. (3)):
  * every query of query tile g of (b,h) attends, with one softmax, to exactly

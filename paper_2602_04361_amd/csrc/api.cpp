@@ -588,8 +588,58 @@ int sparvar_map_index(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t
     return fail(SPARVAR_ERR_CAPACITY, "capacity %lld < bound %lld", (long long)capacity, (long long)need);
   if ((int64_t)(mx + topk) * 2 * 4 * 4 > 64 * 1024)
     return fail(SPARVAR_ERR_UNSUPPORTED, "rows of %d candidates exceed the merge kernel's LDS", mx + topk);
-  return hip_status(launch_map_index(T, S, k, B * H, topk, topk_idx, local_row_ptr, local_col_idx, radius,
-                                     prev_dilation, mx, row_ptr, col_idx, bound, schedule, stream),
+  MapStepArgs sa;
+  sa.k = k;
+  sa.max_local = mx;
+  sa.local_row_ptr = local_row_ptr;
+  sa.local_col_idx = local_col_idx;
+  sa.row_ptr = row_ptr;
+  sa.col_idx = col_idx;
+  return hip_status(launch_map_index(T, S, B * H, topk, topk_idx, radius, prev_dilation, 1, &sa, schedule, stream),
+                    "map index launch");
+}
+
+int sparvar_map_index_steps(const sparvar_geometry_t* g, int32_t S, int32_t n_steps, const int32_t* ks, int32_t B,
+                            int32_t H, int32_t topk, const int32_t* topk_idx, int32_t radius, int32_t prev_dilation,
+                            int32_t* const* row_ptrs, int32_t* const* col_idxs, const int64_t* capacities,
+                            hipStream_t stream) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if (n_steps < 1 || n_steps > kMaxMapSteps)
+    return fail(SPARVAR_ERR_INVALID, "n_steps %d outside [1, %d]", n_steps, kMaxMapSteps);
+  if (!ks || !row_ptrs || !col_idxs || !capacities) return fail(SPARVAR_ERR_INVALID, "a step array is NULL");
+  if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
+  if (topk < 1 || topk > 1024) return fail(SPARVAR_ERR_INVALID, "topk %d outside [1, 1024]", topk);
+  if (radius < 0 || prev_dilation < 0) return fail(SPARVAR_ERR_INVALID, "radius and dilation must be >= 0");
+  if (!topk_idx) return fail(SPARVAR_ERR_INVALID, "topk_idx is NULL");
+  MapStepArgs sa[kMaxMapSteps];
+  int64_t blocks = 0;
+  for (int i = 0; i < n_steps; ++i) {
+    const int32_t k = ks[i];
+    if (S < 1 || k > T.L || S >= k)
+      return fail(SPARVAR_ERR_INVALID, "step %d: need 1 <= S < k <= %d (S=%d, k=%d)", i, T.L, S, k);
+    if (!row_ptrs[i] || !col_idxs[i]) return fail(SPARVAR_ERR_INVALID, "step %d: row_ptr/col_idx is NULL", i);
+    const int32_t mx = local_max_len(T, k, radius, prev_dilation, nullptr);
+    const int64_t rows = (int64_t)B * H * tiles_of(T, k);
+    const int64_t need = rows * (int64_t)(mx + topk) + rows;
+    if (rows >= (int64_t(1) << 31) || need >= (int64_t(1) << 31))
+      return fail(SPARVAR_ERR_INVALID, "step %d: index lists too large for int32 offsets", i);
+    if (capacities[i] < need)
+      return fail(SPARVAR_ERR_CAPACITY, "step %d: capacity %lld < bound %lld", i, (long long)capacities[i],
+                  (long long)need);
+    if ((int64_t)(mx + topk) * 2 * 4 * 4 > 64 * 1024)
+      return fail(SPARVAR_ERR_UNSUPPORTED, "step %d: rows of %d candidates exceed the merge kernel's LDS", i, mx + topk);
+    blocks += (rows + 3) / 4;
+    sa[i].k = k;
+    sa[i].max_local = mx;
+    sa[i].local_row_ptr = nullptr;
+    sa[i].local_col_idx = nullptr;
+    sa[i].row_ptr = row_ptrs[i];
+    sa[i].col_idx = col_idxs[i];
+  }
+  if (blocks >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "too many rows for one launch");
+  return hip_status(launch_map_index(T, S, B * H, topk, topk_idx, radius, prev_dilation, n_steps, sa, nullptr, stream),
                     "map index launch");
 }
 

@@ -1471,7 +1471,8 @@ int32_t max_chunks_per_block(const GeoTable& G, int k, int kc) {
 
 // bf16 grouped launch shapes (d, waves, keys per chunk, pipeline stages).
 #define SV_GROUP_SHAPES(X) \
-  X(128, 8, 64, 2) X(128, 8, 32, 2) X(128, 4, 64, 2) X(128, 4, 32, 2) X(64, 8, 64, 2) X(64, 4, 64, 2)
+  X(128, 8, 64, 2) X(128, 8, 32, 2) X(128, 4, 64, 2) X(128, 4, 32, 2) X(64, 8, 64, 2) X(64, 4, 64, 2) \
+  X(128, 4, 32, 3) X(128, 4, 32, 4)
 
 bool group_shape_exists(int d, int nw, int kc, int ns) {
 #define SV_HAS(DD, NN, KK, SS) \

@@ -58,16 +58,22 @@ __global__ __launch_bounds__(kScanThreads) void local_blocks_kernel(GeoTable G, 
   }
 }
 
-struct MapIO {
-  GeoTable G;
-  const int32_t* topk_idx;
+// One target scale of a map launch; its rows are grid blocks [block0, block0 + ceil(rows / kMapWaves)).
+struct MapStep {
   const int32_t* local_row_ptr;  // NULL: local rows come from (radius, dil)
   const int32_t* local_col;
   int32_t* row_ptr;
   int32_t* col_idx;
-  int32_t* counts;     // [rows] row lengths (only written when a schedule is asked for)
-  int32_t* schedule;   // nullable
-  int32_t S, k, G_k, G_S, topk, rows, max_cand, radius, dil;
+  int32_t* counts;  // [rows] row lengths (only written when a schedule is asked for)
+  int32_t k, G_k, rows, max_cand, block0;
+};
+
+struct MapIO {
+  GeoTable G;
+  const int32_t* topk_idx;
+  int32_t* schedule;  // nullable; single-step launches only
+  int32_t S, G_S, topk, radius, dil, n_steps;
+  MapStep st[kMaxMapSteps];
 };
 
 constexpr int kMapWaves = 4;
@@ -75,43 +81,48 @@ constexpr int32_t kInvalid = 0x7fffffff;
 
 // One wave per row: candidates (local row + mapped selection) in LDS, first
 // occurrences kept, each kept id written at its rank; the row occupies
-// col_idx[r * max_cand, (r + 1) * max_cand) with -1 after its last id.
+// col_idx[r * max_cand, (r + 1) * max_cand) with -1 after its last id. The
+// grid covers the rows of every step of the launch, step after step.
 __global__ __launch_bounds__(kMapWaves * 64) void map_rows_kernel(MapIO io) {
-  extern __shared__ int32_t s_cand[];  // [kMapWaves][2][max_cand]
+  extern __shared__ int32_t s_cand[];  // [kMapWaves][2][max_cand of the step]
+  int si = 0;
+  while (si + 1 < io.n_steps && (int32_t)blockIdx.x >= io.st[si + 1].block0) ++si;
+  const MapStep& ms = io.st[si];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int32_t r = blockIdx.x * kMapWaves + wave;
-  const bool active = r < io.rows;
-  int32_t* cand = s_cand + wave * 2 * io.max_cand;
-  int32_t* uniq = cand + io.max_cand;
+  const int32_t r = ((int32_t)blockIdx.x - ms.block0) * kMapWaves + wave;
+  const bool active = r < ms.rows;
+  const int k = ms.k;
+  int32_t* cand = s_cand + wave * 2 * ms.max_cand;
+  int32_t* uniq = cand + ms.max_cand;
   const GeoTable& G = io.G;
-  const int32_t bh = r / io.G_k, g = r - bh * io.G_k;
-  const int32_t twk = G.Tw[io.k - 1];
+  const int32_t bh = r / ms.G_k, g = r - bh * ms.G_k;
+  const int32_t twk = G.Tw[k - 1];
   const int32_t a = g / twk, c = g - a * twk;
-  const int32_t gs = homography(a, G.Th[io.k - 1], G.Th[io.S - 1]) * G.Tw[io.S - 1] +
+  const int32_t gs = homography(a, G.Th[k - 1], G.Th[io.S - 1]) * G.Tw[io.S - 1] +
                      homography(c, twk, G.Tw[io.S - 1]);
   int32_t lp = 0, n_loc = 0;
-  const LocalRow lr = local_row(G, io.k, io.radius, io.dil, active ? g : 0);
+  const LocalRow lr = local_row(G, k, io.radius, io.dil, active ? g : 0);
   if (active) {
-    if (io.local_row_ptr) {
-      lp = io.local_row_ptr[g];
-      n_loc = io.local_row_ptr[g + 1] - lp;
+    if (ms.local_row_ptr) {
+      lp = ms.local_row_ptr[g];
+      n_loc = ms.local_row_ptr[g + 1] - lp;
     } else {
       n_loc = local_row_len(lr);
     }
     if (n_loc < 0) n_loc = 0;
-    if (n_loc > io.max_cand - io.topk) n_loc = io.max_cand - io.topk;
+    if (n_loc > ms.max_cand - io.topk) n_loc = ms.max_cand - io.topk;
   }
   const int32_t n = active ? n_loc + io.topk : 0;
   const int32_t* sel = io.topk_idx + ((int64_t)bh * io.G_S + gs) * io.topk;
-  const int32_t nb_S = G.NB[io.S], nb_k = G.NB[io.k];
+  const int32_t nb_S = G.NB[io.S], nb_k = G.NB[k];
   for (int32_t i = lane; i < n; i += 64) {
     int32_t v;
     if (i < n_loc) {
-      v = io.local_row_ptr ? io.local_col[lp + i] : local_row_entry(G, io.k, lr, i);
+      v = ms.local_row_ptr ? ms.local_col[lp + i] : local_row_entry(G, k, lr, i);
       if (v < 0 || v >= nb_k) v = kInvalid;
     } else {
       const int32_t s = sel[i - n_loc];
-      v = (s >= 0 && s < nb_S) ? map_block(G, s, io.S, io.k) : kInvalid;
+      v = (s >= 0 && s < nb_S) ? map_block(G, s, io.S, k) : kInvalid;
     }
     cand[i] = v;
   }
@@ -127,7 +138,7 @@ __global__ __launch_bounds__(kMapWaves * 64) void map_rows_kernel(MapIO io) {
   __syncthreads();
   int32_t kept = 0;
   if (active) {
-    int32_t* out = io.col_idx + (int64_t)r * io.max_cand;
+    int32_t* out = ms.col_idx + (int64_t)r * ms.max_cand;
     for (int32_t i = lane; i < n; i += 64) {
       const int32_t v = uniq[i];
       int32_t rank = 0;  // distinct kept values below v
@@ -140,11 +151,11 @@ __global__ __launch_bounds__(kMapWaves * 64) void map_rows_kernel(MapIO io) {
     }
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) kept += __shfl_xor(kept, off, 64);
-    for (int32_t i = kept + lane; i < io.max_cand; i += 64) out[i] = -1;
+    for (int32_t i = kept + lane; i < ms.max_cand; i += 64) out[i] = -1;
     if (lane == 0) {
-      io.row_ptr[r] = r * io.max_cand;
-      if (r == io.rows - 1) io.row_ptr[io.rows] = io.rows * io.max_cand;
-      if (io.schedule) io.counts[r] = kept;
+      ms.row_ptr[r] = r * ms.max_cand;
+      if (r == ms.rows - 1) ms.row_ptr[ms.rows] = ms.rows * ms.max_cand;
+      if (io.schedule) ms.counts[r] = kept;
     }
   }
 }
@@ -174,36 +185,44 @@ hipError_t launch_local_blocks(const GeoTable& G, int k, int32_t radius, int32_t
   return hipGetLastError();
 }
 
-hipError_t launch_map_index(const GeoTable& G, int S, int k, int32_t BH, int32_t topk,
-                            const int32_t* topk_idx, const int32_t* local_row_ptr,
-                            const int32_t* local_col_idx, int32_t radius, int32_t dil, int32_t max_local,
-                            int32_t* row_ptr, int32_t* col_idx, int64_t entries_bound, int32_t* schedule,
+hipError_t launch_map_index(const GeoTable& G, int S, int32_t BH, int32_t topk, const int32_t* topk_idx,
+                            int32_t radius, int32_t dil, int n_steps, const MapStepArgs* steps, int32_t* schedule,
                             hipStream_t stream) {
   MapIO io;
   io.G = G;
   io.topk_idx = topk_idx;
-  io.local_row_ptr = local_row_ptr;
-  io.local_col = local_col_idx;
-  io.row_ptr = row_ptr;
-  io.col_idx = col_idx;
+  io.schedule = n_steps == 1 ? schedule : nullptr;
   io.S = S;
-  io.k = k;
-  io.G_k = tiles_of(G, k);
   io.G_S = tiles_of(G, S);
   io.topk = topk;
-  io.rows = BH * io.G_k;
-  io.max_cand = max_local + topk;
   io.radius = radius;
   io.dil = dil;
-  io.counts = col_idx + entries_bound;  // past the last row slot
-  io.schedule = schedule;
-  if (io.rows == 0) return hipSuccess;
-  const int32_t grid = (io.rows + kMapWaves - 1) / kMapWaves;
-  const size_t shmem = (size_t)kMapWaves * 2 * io.max_cand * sizeof(int32_t);
-  hipLaunchKernelGGL(map_rows_kernel, dim3(grid), dim3(kMapWaves * 64), shmem, stream, io);
+  io.n_steps = n_steps;
+  int32_t blocks = 0, max_cand = 1;
+  for (int i = 0; i < n_steps; ++i) {
+    MapStep& m = io.st[i];
+    const MapStepArgs& a = steps[i];
+    m.local_row_ptr = a.local_row_ptr;
+    m.local_col = a.local_col_idx;
+    m.row_ptr = a.row_ptr;
+    m.col_idx = a.col_idx;
+    m.k = a.k;
+    m.G_k = tiles_of(G, a.k);
+    m.rows = BH * m.G_k;
+    m.max_cand = a.max_local + topk;
+    m.counts = a.col_idx + (int64_t)m.rows * m.max_cand;  // past the last row slot
+    m.block0 = blocks;
+    blocks += (m.rows + kMapWaves - 1) / kMapWaves;
+    max_cand = m.max_cand > max_cand ? m.max_cand : max_cand;
+  }
+  if (blocks == 0) return hipSuccess;
+  const size_t shmem = (size_t)kMapWaves * 2 * max_cand * sizeof(int32_t);
+  hipLaunchKernelGGL(map_rows_kernel, dim3(blocks), dim3(kMapWaves * 64), shmem, stream, io);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || !schedule) return e;
-  hipLaunchKernelGGL(schedule_kernel, dim3(grid), dim3(kMapWaves * 64), 0, stream, io.counts, io.rows, schedule);
+  if (e != hipSuccess || !io.schedule) return e;
+  const int32_t grid = (io.st[0].rows + kMapWaves - 1) / kMapWaves;
+  hipLaunchKernelGGL(schedule_kernel, dim3(grid), dim3(kMapWaves * 64), 0, stream, io.st[0].counts, io.st[0].rows,
+                     schedule);
   return hipGetLastError();
 }
 

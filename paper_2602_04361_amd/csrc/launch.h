@@ -129,10 +129,18 @@ hipError_t launch_topk(const float* scores, int32_t rows, int32_t nb, int32_t to
                        hipStream_t stream);
 hipError_t launch_local_blocks(const GeoTable& G, int k, int32_t radius, int32_t dil, int32_t* row_ptr,
                                int32_t* col_idx, hipStream_t stream);
-hipError_t launch_map_index(const GeoTable& G, int S, int k, int32_t BH, int32_t topk,
-                            const int32_t* topk_idx, const int32_t* local_row_ptr,
-                            const int32_t* local_col_idx, int32_t radius, int32_t dil, int32_t max_local,
-                            int32_t* row_ptr, int32_t* col_idx, int64_t entries_bound, int32_t* schedule,
+// One target scale of a map launch. max_local bounds its local rows; row slots
+// are max_local + topk wide, and the row lengths follow the last slot.
+struct MapStepArgs {
+  int32_t k, max_local;
+  const int32_t *local_row_ptr, *local_col_idx;  // both NULL: generated
+  int32_t *row_ptr, *col_idx;
+};
+constexpr int kMaxMapSteps = 8;
+// Rows of every listed step in one launch; the schedule (single step only) is
+// the longest-first order of that step's rows.
+hipError_t launch_map_index(const GeoTable& G, int S, int32_t BH, int32_t topk, const int32_t* topk_idx,
+                            int32_t radius, int32_t dil, int n_steps, const MapStepArgs* steps, int32_t* schedule,
                             hipStream_t stream);
 
 }  // namespace sparvar

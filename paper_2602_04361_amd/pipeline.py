@@ -7,7 +7,9 @@ current stream:
               call (or, with fused=False, sparvar_dense_attn_fwd followed by
               sparvar_select_blocks);
   step(k):    sparvar_map_index (mapped + local blocks -> CSR + schedule), then
-              sparvar_block_sparse_attn_fwd at scale k.
+              sparvar_block_sparse_attn_fwd at scale k;
+  map_all():  the rows of every step in one sparvar_map_index_steps launch
+              (they depend only on the selection at S).
 Local rows are geometry-only and built once per step by build_local().
 All arithmetic runs in libsparvar.so; this module only allocates and calls.
 """
@@ -85,6 +87,12 @@ class SparsePath:
         rp, ci, sch = self.csr[k]
         sv.sparvar_map_index(self.g, self.S, k, self.B, self.H, self.topk, self.topk_idx, rp_l, ci_l, self.radius,
                              rp, ci, schedule=sch, prev_dilation=self.dil)
+
+    def map_all(self):
+        """The rows of every sparse step in one launch (generated local rows, no schedule)."""
+        sv.sparvar_map_index_steps(self.g, self.S, self.steps, self.B, self.H, self.topk, self.topk_idx, self.radius,
+                                   [self.csr[k][0] for k in self.steps], [self.csr[k][1] for k in self.steps],
+                                   prev_dilation=self.dil)
 
     def attn_step(self, k, Q_all, K_all, V_all, lse=None, use_schedule=True):
         rp, ci, sch = self.csr[k]

@@ -28,6 +28,7 @@ EXPORTS = [
     "sparvar_cs4a_row_stride",
     "sparvar_cs4a_map_tokens",
     "sparvar_cs4a_attn_fwd",
+    "sparvar_map_index_steps",
     "sparvar_csla_row_stride",
     "sparvar_csla_block_rows",
     "sparvar_csla_attn_fwd",
@@ -88,6 +89,7 @@ def load_library(path: str = LIB_PATH):
                                                     f32, vp, vp]),
         "sparvar_cs4a_select_tokens": (ctypes.c_int, [vp, i32, i32, i32, vp, vp]),
         "sparvar_cs4a_row_stride": (i32, [G, i32]),
+        "sparvar_map_index_steps": (ctypes.c_int, [G, i32, i32, vp, i32, i32, i32, vp, i32, i32, vp, vp, vp, vp]),
         "sparvar_csla_row_stride": (i32, [G, i32, i32]),
         "sparvar_csla_block_rows": (ctypes.c_int, [G, i32, vp, i32, vp, i32, vp]),
         "sparvar_csla_attn_fwd": (ctypes.c_int, [G, i32, i32, i32, i32, i32, ctypes.c_int, vp, i64, vp, vp, i64, vp,
@@ -334,6 +336,23 @@ def sparvar_map_index(geom, S, k, B, H, topk, topk_idx, local_row_ptr, local_col
                                             _ptr(local_col_idx), radius, prev_dilation, _ptr(row_ptr),
                                             _ptr(col_idx), col_idx.numel(), _ptr(schedule), _stream(stream)))
     return row_ptr, col_idx, schedule
+
+
+def sparvar_map_index_steps(geom, S, ks, B, H, topk, topk_idx, radius, row_ptrs, col_idxs, prev_dilation=0,
+                            stream=None):
+    """The rows of several target scales in one launch (local rows generated, no schedule)."""
+    n = len(ks)
+    if not (len(row_ptrs) == len(col_idxs) == n):
+        raise SparvarError(ERR_INVALID, "one row_ptr and col_idx per step is required")
+    k_arr = (ctypes.c_int32 * max(n, 1))(*[int(k) for k in ks])
+    rp_arr = (ctypes.c_void_p * max(n, 1))(*[t.data_ptr() for t in row_ptrs])
+    ci_arr = (ctypes.c_void_p * max(n, 1))(*[t.data_ptr() for t in col_idxs])
+    cap_arr = (ctypes.c_int64 * max(n, 1))(*[t.numel() for t in col_idxs])
+    vp = ctypes.c_void_p
+    _check(load_library().sparvar_map_index_steps(geom.ref, S, n, ctypes.cast(k_arr, vp), B, H, topk,
+                                                  _ptr(topk_idx), radius, prev_dilation, ctypes.cast(rp_arr, vp),
+                                                  ctypes.cast(ci_arr, vp), ctypes.cast(cap_arr, vp),
+                                                  _stream(stream)))
 
 
 def sparvar_block_sparse_attn_fwd(geom, k, q_k, k_lek, v_lek, o, row_ptr, col_idx, lse=None, schedule=None,

@@ -183,3 +183,25 @@ def test_csla_validation_before_launch():
     assert attn(kvs=100) == sv.ERR_INVALID
     assert attn(scale=float("nan")) == sv.ERR_INVALID
     assert attn(k=0) == sv.ERR_INVALID
+
+
+def test_map_steps_validation_before_launch():
+    lib = sv.load_library()
+    vp = ctypes.c_void_p
+    fake = 1 << 20
+    g = sv.Geometry(INF, INF, 8, 4)
+    cap = [sv.sparvar_map_index_capacity(g, 10, k, 2, 16, 8, 1) for k in (11, 12, 13)]
+
+    def call(n, ks, caps, S=10, topk=8, rp=fake):
+        k_arr = (ctypes.c_int32 * 3)(*ks)
+        p_arr = (ctypes.c_void_p * 3)(rp, fake, fake)
+        c_arr = (ctypes.c_int64 * 3)(*caps)
+        return lib.sparvar_map_index_steps(g.ref, S, n, ctypes.cast(k_arr, vp), 2, 16, topk, vp(fake), 1, 0,
+                                           ctypes.cast(p_arr, vp), ctypes.cast(p_arr, vp), ctypes.cast(c_arr, vp), None)
+    assert call(0, (11, 12, 13), cap) == sv.ERR_INVALID            # no step
+    assert call(9, (11, 12, 13), cap) == sv.ERR_INVALID            # more than eight
+    assert call(3, (11, 12, 10), cap) == sv.ERR_INVALID            # k <= S
+    assert call(3, (11, 12, 13), cap, topk=0) == sv.ERR_INVALID
+    assert call(3, (11, 12, 13), cap, rp=0) == sv.ERR_INVALID      # NULL row_ptr of step 0
+    assert call(3, (11, 12, 13), (cap[0], cap[1] - 1, cap[2])) == sv.ERR_CAPACITY
+    assert b"step 1" in lib.sparvar_last_error()

@@ -64,6 +64,7 @@ def run_case(h, w, b, ns, S, steps, B, H, d, F, topk, r, dtype, seed=0, dil=0, h
         for t in range(og.tiles(S)):
             assert tk[bh, t].tolist() == O.topk_blocks(scores[bh, t], topk), (bh, t)
 
+    merged = {}
     for kk in steps:
         # local rows: bit-exact
         loc = O.local_blocks(og, kk, r, dil)
@@ -81,6 +82,7 @@ def run_case(h, w, b, ns, S, steps, B, H, d, F, topk, r, dtype, seed=0, dil=0, h
         torch.cuda.synchronize()
         assert csr_rows(rp, ci, padded=True) == got, f"CSR rows (in-call local rows) step {kk}"
         path.local_lists = True
+        merged[kk] = got
         if check_schedule and sch is not None:
             compact_ptr, _ = O.rows_to_csr(got)
             assert sch.cpu().numpy().tolist() == O.longest_first(compact_ptr), f"schedule step {kk}"
@@ -99,6 +101,13 @@ def run_case(h, w, b, ns, S, steps, B, H, d, F, topk, r, dtype, seed=0, dil=0, h
             mx, mean = assert_close(ok[bh][qs], o_ref[qs], dtype, f"sparse O step {kk} head {bh}")
             assert np.abs(lk[bh][qs] - l_ref[qs]).max() <= LSE_TOL[dtype], f"sparse LSE step {kk} head {bh}"
         note(f"  step {kk}: ok (last head max {mx:.2e} mean {mean:.2e})")
+    # every step's rows from one multi-step mapping launch: the same rows
+    for kk in steps:
+        path.csr[kk][1].fill_(-7)
+    path.map_all()
+    torch.cuda.synchronize()
+    for kk in steps:
+        assert csr_rows(path.csr[kk][0], path.csr[kk][1], padded=True) == merged[kk], f"multi-step rows {kk}"
     return path, (Qd, Kd, Vd)
 
 
