@@ -325,8 +325,24 @@ struct TableLds {  // byte offsets inside the table region
   static constexpr int kInfo = kTmask + kTableCap * 4;
   static constexpr int kImask = kInfo + NT * 16;
   static constexpr int kWt = kImask + NT * 4;
-  static constexpr int kBytes = kWt + 16 * 4;
+  static constexpr int kGeo = kWt + 16 * 4;  // LDS copy of the geometry table
+  static constexpr int kBytes = kGeo + (int)((sizeof(GeoTable) + 15) / 16 * 16);
 };
+
+// Copies the geometry table from the kernel arguments into LDS, where the
+// per-thread block decode of a refill reads it: indexed per lane, the
+// kernel-argument copy is read with a chain of dependent global loads (one per
+// scale searched), which made the first refill of every workgroup take
+// microseconds. Visible after the next workgroup barrier.
+template <int NT>
+__device__ __forceinline__ const GeoTable* stage_geometry(const GeoTable& G, char* lds) {
+  static_assert(sizeof(GeoTable) % 4 == 0, "geometry table is 32-bit words");
+  constexpr int kWords = (int)(sizeof(GeoTable) / 4);
+  const int32_t* s = reinterpret_cast<const int32_t*>(&G);
+  int32_t* d = reinterpret_cast<int32_t*>(lds + TableLds<NT>::kGeo);
+  for (int i = threadIdx.x; i < kWords; i += NT) d[i] = s[i];
+  return reinterpret_cast<const GeoTable*>(lds + TableLds<NT>::kGeo);
+}
 
 template <int KC, int NT, class Blocks>
 struct TableCursor {
@@ -519,7 +535,7 @@ struct SparseSrc {
   __device__ __forceinline__ TableCursor<KC, NT, CsrBlocks> table_cursor(int32_t item, char* lds) const {
     const int32_t r = row_of(item);
     TableCursor<KC, NT, CsrBlocks> c;
-    c.G = &G;
+    c.G = stage_geometry<NT>(G, lds);  // the first refill starts with a barrier
     c.blocks.col = col_idx;
     c.blocks.p0 = row_ptr[r];
     c.blocks.p1 = row_ptr[r + 1];
@@ -740,6 +756,7 @@ struct GroupSrc {
     char* glds = lds + TableLds<NT>::kBytes;
     const int T = 1 << lgT;
     const int tid = threadIdx.x;
+    const GeoTable* geo = stage_geometry<NT>(G, lds);  // published by the barrier below
     if (tid < T) {
       int32_t bh, a, c;
       int32_t p = 0, n = 0;
@@ -756,7 +773,7 @@ struct GroupSrc {
     bool long_row = false;
     for (int t = 0; t < T; ++t) long_row |= reinterpret_cast<const int32_t*>(glds + L::kRowN)[t] > RC;
     TableCursor<KC, NT, GroupBlocks<NT>> cur;
-    cur.G = &G;
+    cur.G = geo;
     cur.blocks.col = col_idx;
     cur.blocks.nb = G.NB[k];
     cur.blocks.T = T;

@@ -85,6 +85,16 @@ constexpr int32_t kInvalid = 0x7fffffff;
 // grid covers the rows of every step of the launch, step after step.
 __global__ __launch_bounds__(kMapWaves * 64) void map_rows_kernel(MapIO io) {
   extern __shared__ int32_t s_cand[];  // [kMapWaves][2][max_cand of the step]
+  // The geometry table in LDS: the per-lane decode of local and mapped blocks
+  // indexes it per lane, which on the kernel-argument copy is a chain of
+  // dependent global loads.
+  __shared__ GeoTable s_geo;
+  {
+    const int32_t* src = reinterpret_cast<const int32_t*>(&io.G);
+    int32_t* dst = reinterpret_cast<int32_t*>(&s_geo);
+    for (int i = threadIdx.x; i < (int)(sizeof(GeoTable) / 4); i += kMapWaves * 64) dst[i] = src[i];
+  }
+  __syncthreads();
   int si = 0;
   while (si + 1 < io.n_steps && (int32_t)blockIdx.x >= io.st[si + 1].block0) ++si;
   const MapStep& ms = io.st[si];
@@ -94,7 +104,7 @@ __global__ __launch_bounds__(kMapWaves * 64) void map_rows_kernel(MapIO io) {
   const int k = ms.k;
   int32_t* cand = s_cand + wave * 2 * ms.max_cand;
   int32_t* uniq = cand + ms.max_cand;
-  const GeoTable& G = io.G;
+  const GeoTable& G = s_geo;
   const int32_t bh = r / ms.G_k, g = r - bh * ms.G_k;
   const int32_t twk = G.Tw[k - 1];
   const int32_t a = g / twk, c = g - a * twk;
