@@ -40,6 +40,8 @@ from .cs4a_oracle import token_attention
 from .sparvar_oracle import Geometry
 
 __all__ = [
+    "compact_schedule",
+    "kv_compact",
     "aligned_centre",
     "default_windows",
     "csla_token_mask",
@@ -124,3 +126,19 @@ def csla_attention(q_k, k_lek, v_lek, rows, B, scale):
     n_kv = np.asarray(k_lek).shape[0]
     tok_rows = [[t for v in row for t in range(v * B, min(v * B + B, n_kv))] for row in rows]
     return token_attention(q_k, k_lek, v_lek, tok_rows, B, scale)
+
+
+def compact_schedule(geom: Geometry, keep):
+    """Scale sides of the compressed cache that keeps scales `keep` (ascending,
+    1-based): the kept scales in their order (the sink and local scales of the
+    paper's KV compression)."""
+    keep = [int(l) for l in keep]
+    if not keep or keep != sorted(set(keep)) or keep[0] < 1 or keep[-1] > geom.L:
+        raise ValueError("kept scales must be ascending, distinct and within the schedule")
+    return [geom.hh(l) for l in keep], [geom.ww(l) for l in keep]
+
+
+def kv_compact(x_all, geom: Geometry, keep):
+    """The tokens of the kept scales of one cache plane [N_total, d], in scale order."""
+    x_all = np.asarray(x_all)
+    return np.concatenate([x_all[geom.C(l - 1):geom.C(l)] for l in keep], axis=0)

@@ -10,6 +10,7 @@ import os
 from fractions import Fraction
 
 import numpy as np
+import pytest
 
 import oracle as O
 
@@ -161,3 +162,35 @@ def test_sparsity_differences_match_the_papers_ablation_table():
     gaps = np.array(gaps)
     assert np.ptp(gaps) < 0.35 and gaps.std() < 0.12, gaps
     assert -3.6 < gaps.mean() < -3.0, gaps
+
+
+def test_kv_compression_keeps_the_csla_token_mask():
+    # Keeping only the sink scales and the windowed scales loses no key the token
+    # mask keeps: the mask of the compressed schedule equals the full mask
+    # restricted to the kept scales, and every dropped column of the full mask is
+    # empty (the centres depend only on the sides of the query scale and of the
+    # historical scale).
+    g = O.Geometry(INF, INF, 8, 5)
+    k, ns = 13, 5
+    keep = [1, 2, 3, 4, 5, 11, 12, 13]
+    full = O.csla_token_mask(g, k, ns, O.default_windows(k))
+    h, w = O.compact_schedule(g, keep)
+    assert h == [1, 2, 4, 6, 8, 40, 48, 64] and h == w
+    gc = O.Geometry(h, w, 8, ns)
+    comp = O.csla_token_mask(gc, len(keep), ns, O.default_windows(len(keep)))
+    cols = np.concatenate([np.arange(g.C(l - 1), g.C(l)) for l in keep])
+    assert gc.C(len(keep)) == len(cols) == 121 + 1600 + 2304 + 4096
+    assert np.array_equal(comp, full[:, cols])
+    dropped = np.setdiff1d(np.arange(g.C(k)), cols)
+    assert not full[:, dropped].any()
+    # so token-level attention over the compressed cache equals the full one
+    r = np.random.default_rng(13)
+    x = r.standard_normal((g.C(k), 3))
+    assert np.array_equal(O.kv_compact(x, g, keep), x[cols])
+
+
+def test_compact_schedule_rejects_bad_lists():
+    g = O.Geometry([1, 2, 4], [1, 2, 4], 1, 1)
+    for bad in ([], [2, 1], [1, 1], [0, 1], [1, 4]):
+        with pytest.raises(ValueError):
+            O.compact_schedule(g, bad)
