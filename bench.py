@@ -418,6 +418,64 @@ def sweep_csla(dev, only=None):
                           "speedup_vs_own_dense": t_dense / t_attn}), flush=True)
 
 
+def sweep_kv_compression(dev):
+    """KV compression at the 24-head last-scale shape: keep the sink scales 1-5 and
+    the windowed scales 11-13, copy them into a compact cache (HBM-bound gather:
+    GB/s against 8 TB/s), and run the CSLA block path (blocks of 128) on it."""
+    import torch
+
+    from paper_2602_04361_amd import sparvar as sv
+    from paper_2602_04361_amd.synth import make_qkv
+
+    B, H, d, k, blk = 1, 24, 128, 13, 128
+    keep = [1, 2, 3, 4, 5, 11, 12, 13]
+    n0 = sum(x * x for x in SIDES[:k - 1])
+    n_q, n_kv = SIDES[k - 1] ** 2, n0 + SIDES[k - 1] ** 2
+    q, kk, v = make_qkv(SIDES, SIDES, B, H, d, CFG["n_freq"], 5, seed=100, bf16=True)
+    Q = torch.from_numpy(q[:, :, n0:n_kv]).to(dev).to(torch.bfloat16)
+    K = torch.from_numpy(kk).to(dev).to(torch.bfloat16)
+    V = torch.from_numpy(v).to(dev).to(torch.bfloat16)
+    g = sv.Geometry(SIDES, SIDES, CFG["b"], 5)
+    gc = sv.compact_geometry(g, keep)
+    m = sum(SIDES[l - 1] ** 2 for l in keep)
+    Kc = torch.empty(B, H, m, d, dtype=torch.bfloat16, device=dev)
+    Vc = torch.empty_like(Kc)
+    o = torch.empty_like(Q)
+    stream = torch.cuda.current_stream()
+
+    def timed(fn, n=20):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        for a, b in evs:
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        return float(np.median([a.elapsed_time(b) for a, b in evs]))
+
+    t_copy = timed(lambda: sv.sparvar_kv_compact(g, keep, K, V, Kc, Vc))
+    copy_bytes = 2.0 * 2 * B * H * m * d * 2  # K and V, read and written
+    kc = len(keep)
+    wins = [0] * (kc - 3) + [3, 5, 7]
+    M = sv.sparvar_csla_row_stride(gc, kc, blk)
+    rows = torch.empty(-(-n_q // blk), M, dtype=torch.int32, device=dev)
+    sv.sparvar_csla_block_rows(gc, kc, wins, blk, rows)
+    t_attn = timed(lambda: sv.sparvar_csla_attn_fwd(gc, kc, blk, Q, Kc, Vc, o, rows))
+    r = rows.cpu().numpy()
+    pairs = sum(min(blk, n_q - u * blk) * sum(min(blk, m - x * blk) for x in r[u][r[u] >= 0]) for u in range(len(r)))
+    flops = 4.0 * d * B * H * pairs
+    print(json.dumps({"sweep": "kv_compression_sink5_local3_b128", "B": B, "H": H, "kept_scales": keep,
+                      "kv_tokens_full": n_kv, "kv_tokens_kept": m,
+                      "kv_bytes_full": 2 * B * H * n_kv * d * 2, "kv_bytes_kept": 2 * B * H * m * d * 2,
+                      "compact_ms": t_copy, "compact_gbs": copy_bytes / t_copy / 1e6,
+                      "compact_frac_hbm_peak": copy_bytes / t_copy / 1e6 / 8000.0,
+                      "attn_ms": t_attn, "tflops": flops / t_attn / 1e9,
+                      "frac_bf16_peak": flops / t_attn / 1e9 / PEAK_BF16_TFLOPS,
+                      "density_of_compact": pairs / (n_q * m)}), flush=True)
+
+
 # ---------------------------------------------------------------- main
 def main():
     args = parse()
@@ -440,9 +498,11 @@ def main():
         sweep(args, dev)
         sweep_cs4a(dev)
         sweep_csla(dev)
+        sweep_kv_compression(dev)
         return
     if args.csla:
         sweep_csla(dev)
+        sweep_kv_compression(dev)
         return
     B, H, d = CFG["B"], CFG["H"], CFG["d"]
     BH = B * H

@@ -364,6 +364,26 @@ int sparvar_csla_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t block,
                           int64_t kv_bh_stride, void* o, float* lse, float softmax_scale,
                           const int32_t* rows, int32_t M, hipStream_t stream);
 
+/*
+ * KV compression, the memory side of the paper's "+ KV comp." setting (memory
+ * consumption paragraph of the additional experiments: keep only the KV cache
+ * of the sink scales and of the local scales). For every (b,h) plane, copies
+ * the K and V tokens of the scales keep[0..n_keep) (1-based, strictly
+ * ascending), in that order, into a compact cache: the cache of the schedule
+ * made of the kept scales' sides, on which every call above runs unchanged.
+ * With the sink scales and the scales that carry CSLA windows kept, the CSLA
+ * token mask of the compact schedule is exactly the full mask restricted to the
+ * kept tokens (dropped scales hold no kept key).
+ *   keep: host int32 [n_keep], read during the call.
+ *   k_src, v_src: [B,H,>= C_{keep[n_keep-1]},d] (plane stride src_bh_stride);
+ *   k_dst, v_dst: [B,H,>= sum of N_l over the kept scales,d] (plane stride
+ *   dst_bh_stride); element strides are multiples of 16 bytes. B*H <= 65535.
+ */
+int sparvar_kv_compact(const sparvar_geometry_t* g, int32_t n_keep, const int32_t* keep, int32_t B,
+                       int32_t H, int32_t d, sparvar_dtype_t dtype, const void* k_src,
+                       const void* v_src, int64_t src_bh_stride, void* k_dst, void* v_dst,
+                       int64_t dst_bh_stride, hipStream_t stream);
+
 /* Static description of a status code. */
 const char* sparvar_status_string(int status);
 /* Message of the last failed call on this thread ("" if none). */

@@ -17,7 +17,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libsparvar.so")
-SOURCES = ["attention.hip", "select.hip", "decision.hip", "cs4a.hip", "csla.hip", "index.hip", "api.cpp"]
+SOURCES = ["attention.hip", "select.hip", "decision.hip", "cs4a.hip", "csla.hip", "kv.hip", "index.hip", "api.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -518,6 +518,45 @@ int sparvar_csla_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t block,
   return hip_status(launch_block_row_attn(a, stream), "CSLA attention launch");
 }
 
+int sparvar_kv_compact(const sparvar_geometry_t* g, int32_t n_keep, const int32_t* keep, int32_t B, int32_t H,
+                       int32_t d, sparvar_dtype_t dtype, const void* k_src, const void* v_src, int64_t src_bh_stride,
+                       void* k_dst, void* v_dst, int64_t dst_bh_stride, hipStream_t stream) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if ((st = check_dtype_d(dtype, d))) return st;
+  if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
+  if (!keep || n_keep < 1 || n_keep > T.L) return fail(SPARVAR_ERR_INVALID, "n_keep %d outside [1, %d]", n_keep, T.L);
+  for (int i = 0; i < n_keep; ++i) {
+    if (keep[i] < 1 || keep[i] > T.L || (i > 0 && keep[i] <= keep[i - 1]))
+      return fail(SPARVAR_ERR_INVALID, "kept scales must be strictly ascending within [1, %d]", T.L);
+  }
+  const int elem = dtype == SPARVAR_BF16 ? 2 : 4;
+  int64_t kept = 0;
+  for (int i = 0; i < n_keep; ++i) kept += T.C[keep[i]] - T.C[keep[i] - 1];
+  const int32_t need_src = T.C[keep[n_keep - 1]];
+  if ((st = check_plane(k_src, src_bh_stride, need_src, d, elem, "k_src"))) return st;
+  if ((st = check_plane(v_src, src_bh_stride, need_src, d, elem, "v_src"))) return st;
+  if ((st = check_plane(k_dst, dst_bh_stride, kept, d, elem, "k_dst"))) return st;
+  if ((st = check_plane(v_dst, dst_bh_stride, kept, d, elem, "v_dst"))) return st;
+  if (kept * d * elem / 16 >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "compact plane too large");
+  if ((int64_t)B * H > 65535) return fail(SPARVAR_ERR_INVALID, "B*H above 65535");
+  KvCompactArgs a;
+  a.G = &T;
+  a.n_keep = n_keep;
+  a.keep = keep;
+  a.planes = B * H;
+  a.d = d;
+  a.elem = elem;
+  a.k_src = k_src;
+  a.v_src = v_src;
+  a.k_dst = k_dst;
+  a.v_dst = v_dst;
+  a.src_bh_stride = src_bh_stride;
+  a.dst_bh_stride = dst_bh_stride;
+  return hip_status(launch_kv_compact(a, stream), "KV compaction launch");
+}
+
 int64_t sparvar_local_blocks_capacity(const sparvar_geometry_t* g, int32_t k, int32_t radius,
                                       int32_t prev_dilation) {
   GeoTable T;

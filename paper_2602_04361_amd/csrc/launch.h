@@ -112,6 +112,18 @@ struct BlockRowAttnArgs {
 // Key blocks a 1-D block row may list (LDS bitmask of the row builder).
 constexpr int32_t kCslaMaxBlocks = 2048;
 
+// Copy of the kept scales' K/V tokens (in scale order) into a compact cache.
+struct KvCompactArgs {
+  const GeoTable* G;
+  int32_t n_keep;
+  const int32_t* keep;  // host, 1-based, ascending
+  int32_t planes, d, elem;
+  const void *k_src, *v_src;
+  void *k_dst, *v_dst;
+  int64_t src_bh_stride, dst_bh_stride;  // elements
+};
+hipError_t launch_kv_compact(const KvCompactArgs& a, hipStream_t stream);
+
 hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream);
 hipError_t launch_block_row_attn(const BlockRowAttnArgs& a, hipStream_t stream);
 hipError_t launch_csla_rows(const GeoTable& G, int k, const int32_t* windows, int32_t B, int32_t* rows, int32_t M,

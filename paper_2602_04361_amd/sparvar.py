@@ -29,6 +29,7 @@ EXPORTS = [
     "sparvar_cs4a_map_tokens",
     "sparvar_cs4a_attn_fwd",
     "sparvar_map_index_steps",
+    "sparvar_kv_compact",
     "sparvar_csla_row_stride",
     "sparvar_csla_block_rows",
     "sparvar_csla_attn_fwd",
@@ -90,6 +91,7 @@ def load_library(path: str = LIB_PATH):
         "sparvar_cs4a_select_tokens": (ctypes.c_int, [vp, i32, i32, i32, vp, vp]),
         "sparvar_cs4a_row_stride": (i32, [G, i32]),
         "sparvar_map_index_steps": (ctypes.c_int, [G, i32, i32, vp, i32, i32, i32, vp, i32, i32, vp, vp, vp, vp]),
+        "sparvar_kv_compact": (ctypes.c_int, [G, i32, vp, i32, i32, i32, ctypes.c_int, vp, vp, i64, vp, vp, i64, vp]),
         "sparvar_csla_row_stride": (i32, [G, i32, i32]),
         "sparvar_csla_block_rows": (ctypes.c_int, [G, i32, vp, i32, vp, i32, vp]),
         "sparvar_csla_attn_fwd": (ctypes.c_int, [G, i32, i32, i32, i32, i32, ctypes.c_int, vp, i64, vp, vp, i64, vp,
@@ -277,6 +279,27 @@ def sparvar_cs4a_attn_fwd(geom, k, C, q_k, k_lek, v_lek, o, tokens, M, lse=None,
                                      _scale(softmax_scale, d), _ptr(tokens), M, mode, _ptr(base), base_scale,
                                      _stream(stream)))
     return o
+
+
+def sparvar_kv_compact(geom, keep, k_src, v_src, k_dst, v_dst, stream=None):
+    """Copy the K/V tokens of the kept scales (1-based, ascending) into a compact cache; see sparvar.h."""
+    B, H, _, d = k_src.shape
+    if _plane_stride(v_src, "v_src") != _plane_stride(k_src, "k_src") or \
+            _plane_stride(v_dst, "v_dst") != _plane_stride(k_dst, "k_dst"):
+        raise SparvarError(ERR_INVALID, "K and V must share plane strides")
+    arr = (ctypes.c_int32 * max(len(keep), 1))(*[int(l) for l in keep])
+    _check(load_library().sparvar_kv_compact(geom.ref, len(keep), ctypes.cast(arr, ctypes.c_void_p), B, H, d,
+                                             _dtype_code(k_src), _ptr(k_src), _ptr(v_src),
+                                             _plane_stride(k_src, "k_src"), _ptr(k_dst), _ptr(v_dst),
+                                             _plane_stride(k_dst, "k_dst"), _stream(stream)))
+    return k_dst, v_dst
+
+
+def compact_geometry(geom, keep, num_sink_scales=None):
+    """Geometry of the compact cache that keeps scales `keep` (its scales are the kept ones, in order)."""
+    keep = [int(l) for l in keep]
+    ns = geom.num_sink_scales if num_sink_scales is None else num_sink_scales
+    return Geometry([geom.h[l - 1] for l in keep], [geom.w[l - 1] for l in keep], geom.block_edge, ns)
 
 
 def sparvar_csla_row_stride(geom, k, block):

@@ -205,3 +205,24 @@ def test_map_steps_validation_before_launch():
     assert call(3, (11, 12, 13), cap, rp=0) == sv.ERR_INVALID      # NULL row_ptr of step 0
     assert call(3, (11, 12, 13), (cap[0], cap[1] - 1, cap[2])) == sv.ERR_CAPACITY
     assert b"step 1" in lib.sparvar_last_error()
+
+
+def test_kv_compact_validation_before_launch():
+    lib = sv.load_library()
+    vp = ctypes.c_void_p
+    fake = vp(1 << 20)
+    g = sv.Geometry(INF, INF, 8, 5)
+
+    def call(keep, d=128, dt=sv.BF16, src=10521 * 128, dst=8121 * 128):
+        arr = (ctypes.c_int32 * max(len(keep), 1))(*keep)
+        return lib.sparvar_kv_compact(g.ref, len(keep), ctypes.cast(arr, vp), 1, 24, d, dt, fake, fake, src, fake,
+                                      fake, dst, None)
+    keep = [1, 2, 3, 4, 5, 11, 12, 13]
+    assert call([]) == sv.ERR_INVALID
+    assert call([1, 3, 2]) == sv.ERR_INVALID               # not ascending
+    assert call([0, 1]) == sv.ERR_INVALID                  # scale out of range
+    assert call([1, 14]) == sv.ERR_INVALID
+    assert call(keep, d=96) == sv.ERR_UNSUPPORTED
+    assert call(keep, dst=8120 * 128) == sv.ERR_INVALID    # compact plane too short
+    assert call(keep, src=10520 * 128) == sv.ERR_INVALID   # source plane too short for scale 13
+    assert sv.compact_geometry(g, keep).h == [1, 2, 4, 6, 8, 40, 48, 64]
