@@ -279,19 +279,28 @@ int sparvar_map_index(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t
  * n_steps (1 <= n_steps <= 8), the rows of scale ks[i] exactly as
  * sparvar_map_index(g, S, ks[i], B, H, topk, topk_idx, NULL, NULL, radius,
  * prev_dilation, row_ptrs[i], col_idxs[i], capacities[i], NULL, stream) writes
- * them (local rows generated in the call, no schedule). The mapping of every
- * later scale depends only on the selection at S, so all of them can be built
- * right after the decision step.
+ * them (local rows generated in the call). The mapping of every later scale
+ * depends only on the selection at S, so all of them can be built right after
+ * the decision step.
  *   ks, row_ptrs, col_idxs, capacities: host arrays of n_steps entries, read
  *   during the call; row_ptrs[i], col_idxs[i] are device buffers sized as for
  *   sparvar_map_index, capacities[i] >= sparvar_map_index_capacity(g, S,
  *   ks[i], B, H, topk, radius, prev_dilation).
+ *   orders (nullable host array of n_steps nullable device pointers, each
+ *   int32 [B*H*G_k of ks[i]]): a launch order for sparvar_block_sparse_attn_fwd
+ *   at ks[i] (its schedule argument), written from the row lengths by a second
+ *   launch: the work items of the form that call uses by default on this
+ *   device (one query tile per workgroup, or groups of neighbouring tiles),
+ *   longest first inside each XCD's share of the launch. Tile items are stored
+ *   as row ids, group items g as -2 - g; the attention call uses an order only
+ *   for the form it belongs to and launches in natural order otherwise. The
+ *   order never changes results.
  */
 int sparvar_map_index_steps(const sparvar_geometry_t* g, int32_t S, int32_t n_steps, const int32_t* ks,
                             int32_t B, int32_t H, int32_t topk, const int32_t* topk_idx,
                             int32_t radius, int32_t prev_dilation, int32_t* const* row_ptrs,
                             int32_t* const* col_idxs, const int64_t* capacities,
-                            hipStream_t stream);
+                            int32_t* const* orders, hipStream_t stream);
 
 /*
  * Block-sparse cross-scale attention at scale k (the sparse update
@@ -306,9 +315,13 @@ int sparvar_map_index_steps(const sparvar_geometry_t* g, int32_t S, int32_t n_st
  *   strictly ascending (as written by sparvar_map_index). A row that repeats
  *   an id or lists ids out of order gives unspecified values (never an access
  *   outside the inputs and outputs).
- *   schedule (nullable): a permutation of the rows giving the launch order
- *   of the one-tile-per-workgroup form; it changes only the order of work,
- *   never the results (the form that groups neighbouring tiles ignores it).
+ *   schedule (nullable): a launch order; it changes only the order of work,
+ *   never the results. Either a permutation of the B*H*G_k rows (non-negative
+ *   entries: sparvar_map_index's longest-first schedule, or an order from
+ *   sparvar_map_index_steps), used by the one-tile-per-workgroup form, or an
+ *   order of groups of neighbouring tiles (entries -2 - group, from
+ *   sparvar_map_index_steps), used by the grouped form; each form launches in
+ *   natural order when given the other kind (told apart by schedule[0]).
  */
 int sparvar_block_sparse_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t B, int32_t H,
                                   int32_t d, sparvar_dtype_t dtype, const void* q_k,

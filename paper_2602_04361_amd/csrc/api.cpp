@@ -641,7 +641,7 @@ int sparvar_map_index(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t
 int sparvar_map_index_steps(const sparvar_geometry_t* g, int32_t S, int32_t n_steps, const int32_t* ks, int32_t B,
                             int32_t H, int32_t topk, const int32_t* topk_idx, int32_t radius, int32_t prev_dilation,
                             int32_t* const* row_ptrs, int32_t* const* col_idxs, const int64_t* capacities,
-                            hipStream_t stream) {
+                            int32_t* const* orders, hipStream_t stream) {
   GeoTable T;
   int st = build_table(g, &T);
   if (st) return st;
@@ -678,8 +678,12 @@ int sparvar_map_index_steps(const sparvar_geometry_t* g, int32_t S, int32_t n_st
     sa[i].col_idx = col_idxs[i];
   }
   if (blocks >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "too many rows for one launch");
-  return hip_status(launch_map_index(T, S, B * H, topk, topk_idx, radius, prev_dilation, n_steps, sa, nullptr, stream),
-                    "map index launch");
+  st = hip_status(launch_map_index(T, S, B * H, topk, topk_idx, radius, prev_dilation, n_steps, sa, nullptr, stream),
+                  "map index launch");
+  if (st || !orders) return st;
+  return hip_status(launch_map_order(T, B * H, topk, n_steps, sa, orders, device_cus(),
+                                     env_int("SPARVAR_SPARSE_GROUP_WAVES", -1), stream),
+                    "launch order launch");
 }
 
 int sparvar_block_sparse_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t B, int32_t H,

@@ -488,8 +488,8 @@ struct SparseSrc {
   GeoTable G;
   const int32_t* row_ptr;
   const int32_t* col_idx;
-  const int32_t* schedule;
-  int32_t k, G_k, slabs, q_per_wg;
+  const int32_t* schedule;  // nullable launch order of rows; ignored when schedule[0] < 0 (an order of groups)
+  int32_t k, G_k, slabs, q_per_wg, n_rows;
   int32_t max_chunks_per_block;  // bound used to size a table refill
 
   template <int NT>
@@ -497,7 +497,9 @@ struct SparseSrc {
   __device__ __forceinline__ int tile_of(int) const { return 0; }
   __device__ __forceinline__ int32_t row_of(int32_t item) const {
     const int32_t r = item / slabs;
-    return schedule ? schedule[r] : r;
+    if (!schedule || schedule[0] < 0) return r;
+    const int32_t v = schedule[r];
+    return (v >= 0 && v < n_rows) ? v : r;
   }
   __device__ __forceinline__ QuerySet queries(int32_t item, int wave) const {
     const int32_t r = row_of(item);
@@ -724,6 +726,17 @@ struct GroupSrc {
   int32_t ngc, n_groups;  // groups per group row, groups per (b, h)
   uint32_t wave_tile, wave_slab;  // 4 bits per wave: the wave's tile in the group and its 32-query slab
   int32_t max_chunks_per_block;
+  // Nullable launch order: order[p] = -2 - (group item launched at position p),
+  // as the mapping call writes it; a row permutation (non-negative entries) is
+  // not an order of groups and is ignored.
+  const int32_t* order;
+  static constexpr bool kRemap = true;
+
+  __device__ __forceinline__ int32_t remap(int32_t p, int32_t n_items) const {
+    if (!order || order[0] >= 0) return p;
+    const int32_t v = -2 - order[p];
+    return (v >= 0 && v < n_items) ? v : p;
+  }
 
   template <int NT>
   static constexpr int table_bytes() { return TableLds<NT>::kBytes + GroupLds<NT>::kBytes; }
@@ -818,6 +831,11 @@ template <class Src, class = void>
 constexpr bool kRunsOf = false;
 template <class Src>
 constexpr bool kRunsOf<Src, std::void_t<decltype(Src::kRuns)>> = Src::kRuns;
+// Sources with a kRemap member map a launch position to a work item (GroupSrc).
+template <class Src, class = void>
+constexpr bool kRemapOf = false;
+template <class Src>
+constexpr bool kRemapOf<Src, std::void_t<decltype(Src::kRemap)>> = Src::kRemap;
 
 // ---------------------------------------------------------------- bf16 kernel
 template <int D, int NW, int KC, int NS, class Src>
@@ -837,8 +855,9 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
   constexpr int kTblBytes = Src::template table_bytes<NT>();
   __shared__ __attribute__((aligned(16))) char tsmem[kTblBytes];
 
-  const int32_t item = swizzled_item(blockIdx.x, gridDim.x, io.swizzle);
+  int32_t item = swizzled_item(blockIdx.x, gridDim.x, io.swizzle);
   if (item >= io.n_items) return;
+  if constexpr (kRemapOf<Src>) item = __builtin_amdgcn_readfirstlane(src.remap(item, io.n_items));
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -1568,6 +1587,7 @@ hipError_t launch_grouped(const SparseAttnArgs& a, int nw, int wpt, int kc, int 
   proto.n_groups = ngr * ngc;
   wave_map(nw, T, wpt, &proto.wave_tile, &proto.wave_slab);
   proto.max_chunks_per_block = max_chunks_per_block(G, k, kc);
+  proto.order = a.schedule;
   auto as = [&](auto tag) {
     decltype(tag) s;
     s.G = proto.G;
@@ -1583,6 +1603,7 @@ hipError_t launch_grouped(const SparseAttnArgs& a, int nw, int wpt, int kc, int 
     s.wave_tile = proto.wave_tile;
     s.wave_slab = proto.wave_slab;
     s.max_chunks_per_block = proto.max_chunks_per_block;
+    s.order = proto.order;
     return s;
   };
 #define SV_GROUP(DD, NN, KK, SS) \
@@ -1594,6 +1615,30 @@ hipError_t launch_grouped(const SparseAttnArgs& a, int nw, int wpt, int kc, int 
 
 }  // namespace
 
+int group_waves_for(const GeoTable& G, int k, int32_t BH, int num_cu, int group_waves) {
+  if (group_waves >= 0) return group_waves;
+  const int wpt = waves_for(G.eh[k - 1] * G.ew[k - 1]);
+  if (wpt > 2) return 0;
+  const int32_t gh = wpt == 2 ? 1 : 2, gw = 2;  // 1 x 2 or 2 x 2 tiles
+  const int64_t groups = (int64_t)BH * ((G.Th[k - 1] + gh - 1) / gh) * ((G.Tw[k - 1] + gw - 1) / gw);
+  return groups >= 4 * (int64_t)num_cu ? 4 : 0;
+}
+
+SparseForm sparse_form(const GeoTable& G, int k, int32_t BH, int num_cu, int group_waves) {
+  SparseForm f;
+  const int wpt = waves_for(G.eh[k - 1] * G.ew[k - 1]);
+  const int gwv = group_waves_for(G, k, BH, num_cu, group_waves);
+  f.gh = f.gw = 0;
+  f.n_items = BH * tiles_of(G, k);
+  if (gwv > wpt) {
+    const int T = gwv / wpt;
+    f.gh = T == 2 ? 1 : 2;
+    f.gw = T == 8 ? 4 : 2;
+    f.n_items = BH * ((G.Th[k - 1] + f.gh - 1) / f.gh) * ((G.Tw[k - 1] + f.gw - 1) / f.gw);
+  }
+  return f;
+}
+
 hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream) {
   const GeoTable& G = *a.G;
   const int k = a.k;
@@ -1604,15 +1649,7 @@ hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream) {
   // 4-wave workgroups, when that still gives every CU at least four workgroups;
   // with fewer, the last round of workgroups runs the chip part-empty and one
   // tile per workgroup is faster.
-  int gwv = a.group_waves;
-  if (gwv < 0) {
-    gwv = 0;
-    if (wpt <= 2) {
-      const int32_t gh = wpt == 2 ? 1 : 2, gw = 2;  // 1 x 2 or 2 x 2 tiles
-      const int64_t groups = (int64_t)a.BH * ((G.Th[k - 1] + gh - 1) / gh) * ((G.Tw[k - 1] + gw - 1) / gw);
-      if (groups >= 4 * (int64_t)a.num_cu) gwv = 4;
-    }
-  }
+  const int gwv = group_waves_for(G, k, a.BH, a.num_cu, a.group_waves);
   if (a.bf16 && a.waves <= 0 && gwv > wpt) {
     int kc = a.group_chunk, ns = a.group_stages;
     if (!group_shape_exists(a.d, gwv, kc, ns)) {
@@ -1651,6 +1688,7 @@ hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream) {
     s.G_k = G_k;
     s.q_per_wg = qpw;
     s.slabs = slabs;
+    s.n_rows = a.BH * G_k;
     return s;
   };
   return dispatch<SparseSrc>(a.bf16, a.d, nw, kc, ns, io, make, stream);

@@ -64,7 +64,7 @@ struct MapStep {
   const int32_t* local_col;
   int32_t* row_ptr;
   int32_t* col_idx;
-  int32_t* counts;  // [rows] row lengths (only written when a schedule is asked for)
+  int32_t* counts;  // [rows] row lengths
   int32_t k, G_k, rows, max_cand, block0;
 };
 
@@ -165,7 +165,7 @@ __global__ __launch_bounds__(kMapWaves * 64) void map_rows_kernel(MapIO io) {
     if (lane == 0) {
       ms.row_ptr[r] = r * ms.max_cand;
       if (r == ms.rows - 1) ms.row_ptr[ms.rows] = ms.rows * ms.max_cand;
-      if (io.schedule) ms.counts[r] = kept;
+      ms.counts[r] = kept;
     }
   }
 }
@@ -192,6 +192,93 @@ hipError_t launch_local_blocks(const GeoTable& G, int k, int32_t radius, int32_t
                                int32_t* col_idx, hipStream_t stream) {
   hipLaunchKernelGGL(local_blocks_kernel, dim3(1), dim3(kScanThreads), 0, stream, G, k, radius, dil, row_ptr,
                      col_idx);
+  return hipGetLastError();
+}
+
+// Launch order of the block-sparse kernel's work items (query tiles, or groups
+// of neighbouring tiles) at one step: inside each XCD's share of the launch
+// positions (the items the XCD-aware order gives that XCD), items go longest
+// first (length = the rows' entries, summed over a group's tiles; ties keep the
+// item order), so the workgroups that start last are the short ones.
+struct OrderStep {
+  int32_t* order;
+  const int32_t* counts;
+  int32_t n_items, per;                      // items, and positions per XCD share
+  int32_t G_k, Th, Tw, gh, gw, ngc, n_groups;  // gh = 0: items are rows
+};
+
+struct OrderIO {
+  OrderStep st[kMaxMapSteps];
+};
+
+constexpr int kOrderThreads = 256;
+constexpr int kOrderMaxPer = 4096;
+
+// Grid (8 XCD shares, steps); one workgroup ranks one share.
+__global__ __launch_bounds__(kOrderThreads) void order_kernel(OrderIO io) {
+  __shared__ int32_t key[kOrderMaxPer];
+  const OrderStep& s = io.st[blockIdx.y];
+  const int32_t lo = (int32_t)blockIdx.x * s.per;
+  const int32_t hi = lo + s.per < s.n_items ? lo + s.per : s.n_items;
+  const int32_t n = hi - lo;
+  if (n <= 0) return;
+  const bool grouped = s.gh > 0;
+  if (n > kOrderMaxPer) {  // beyond the LDS table: the natural order
+    for (int32_t i = lo + (int32_t)threadIdx.x; i < hi; i += kOrderThreads) s.order[i] = grouped ? -2 - i : i;
+    return;
+  }
+  for (int32_t i = threadIdx.x; i < n; i += kOrderThreads) {
+    const int32_t it = lo + i;
+    int32_t len;
+    if (!grouped) {
+      len = s.counts[it];
+    } else {
+      const int32_t bh = it / s.n_groups, gi = it - bh * s.n_groups;
+      const int32_t A = gi / s.ngc, Cg = gi - A * s.ngc;
+      len = 0;
+      for (int t = 0; t < s.gh * s.gw; ++t) {
+        const int32_t a = A * s.gh + t / s.gw, c = Cg * s.gw + t % s.gw;
+        if (a < s.Th && c < s.Tw) len += s.counts[bh * s.G_k + a * s.Tw + c];
+      }
+    }
+    key[i] = len;
+  }
+  __syncthreads();
+  for (int32_t i = threadIdx.x; i < n; i += kOrderThreads) {
+    const int32_t ki = key[i];
+    int32_t rank = 0;
+    for (int32_t j = 0; j < n; ++j) {
+      const int32_t kj = key[j];
+      rank += (kj > ki) | ((kj == ki) & (j < i));
+    }
+    s.order[lo + rank] = grouped ? -2 - (lo + i) : lo + i;
+  }
+}
+
+hipError_t launch_map_order(const GeoTable& G, int32_t BH, int32_t topk, int n_steps, const MapStepArgs* steps,
+                            int32_t* const* orders, int num_cu, int group_waves, hipStream_t stream) {
+  OrderIO io;
+  int used = 0;
+  for (int i = 0; i < n_steps; ++i) {
+    OrderStep& o = io.st[i];
+    const int k = steps[i].k;
+    const SparseForm f = sparse_form(G, k, BH, num_cu, group_waves);
+    const int32_t rows = BH * tiles_of(G, k);
+    o.order = orders ? orders[i] : nullptr;
+    o.counts = steps[i].col_idx + (int64_t)rows * (steps[i].max_local + topk);  // the row lengths after the slots
+    o.n_items = o.order ? f.n_items : 0;
+    o.per = (o.n_items + 7) / 8;
+    o.G_k = tiles_of(G, k);
+    o.Th = G.Th[k - 1];
+    o.Tw = G.Tw[k - 1];
+    o.gh = f.gh;
+    o.gw = f.gw;
+    o.ngc = f.gw > 0 ? (G.Tw[k - 1] + f.gw - 1) / f.gw : 1;
+    o.n_groups = f.gh > 0 ? ((G.Th[k - 1] + f.gh - 1) / f.gh) * o.ngc : 1;
+    if (o.order) ++used;
+  }
+  if (used == 0) return hipSuccess;
+  hipLaunchKernelGGL(order_kernel, dim3(8, n_steps), dim3(kOrderThreads), 0, stream, io);
   return hipGetLastError();
 }
 

@@ -124,6 +124,16 @@ struct KvCompactArgs {
 };
 hipError_t launch_kv_compact(const KvCompactArgs& a, hipStream_t stream);
 
+// Work items of the bf16 block-sparse launch at scale k (with the default
+// waves, chunk and stages): one query tile per workgroup (gh = gw = 0), or groups
+// of gh x gw neighbouring tiles per workgroup. group_waves: as in SparseAttnArgs.
+struct SparseForm {
+  int gh, gw;
+  int32_t n_items;
+};
+int group_waves_for(const GeoTable& G, int k, int32_t BH, int num_cu, int group_waves);
+SparseForm sparse_form(const GeoTable& G, int k, int32_t BH, int num_cu, int group_waves);
+
 hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream);
 hipError_t launch_block_row_attn(const BlockRowAttnArgs& a, hipStream_t stream);
 hipError_t launch_csla_rows(const GeoTable& G, int k, const int32_t* windows, int32_t B, int32_t* rows, int32_t M,
@@ -154,5 +164,10 @@ constexpr int kMaxMapSteps = 8;
 hipError_t launch_map_index(const GeoTable& G, int S, int32_t BH, int32_t topk, const int32_t* topk_idx,
                             int32_t radius, int32_t dil, int n_steps, const MapStepArgs* steps, int32_t* schedule,
                             hipStream_t stream);
+// Launch order of the block-sparse kernel at each step with a non-NULL orders[i]
+// (from the row lengths the map launch wrote): XCD-local longest first, over the
+// work items of the form sparse_form() gives; group items are stored as -2 - item.
+hipError_t launch_map_order(const GeoTable& G, int32_t BH, int32_t topk, int n_steps, const MapStepArgs* steps,
+                            int32_t* const* orders, int num_cu, int group_waves, hipStream_t stream);
 
 }  // namespace sparvar

@@ -57,6 +57,7 @@ class SparsePath:
             self.csr[k] = (torch.empty(rows + 1, **i32), torch.empty(cap, **i32),
                            torch.empty(rows, **i32) if use_schedule else None)
             self.out[k] = torch.empty(B, H, ik["n_tokens"], d, dtype=dtype, device=device)
+        self.orders = {}
 
     # ------------------------------------------------------------------ calls
     def build_local(self):
@@ -88,14 +89,22 @@ class SparsePath:
         sv.sparvar_map_index(self.g, self.S, k, self.B, self.H, self.topk, self.topk_idx, rp_l, ci_l, self.radius,
                              rp, ci, schedule=sch, prev_dilation=self.dil)
 
-    def map_all(self):
-        """The rows of every sparse step in one launch (generated local rows, no schedule)."""
+    def map_all(self, orders=False):
+        """The rows of every sparse step in one launch (generated local rows); with orders, also each step's
+        attention launch order (longest first inside each XCD's share), used by attn_step(use_order=True)."""
+        if orders and not self.orders:
+            i32 = dict(dtype=torch.int32, device=self.device)
+            self.orders = {k: torch.empty(self.B * self.H * self.info[k]["tiles_h"] * self.info[k]["tiles_w"], **i32)
+                           for k in self.steps}
         sv.sparvar_map_index_steps(self.g, self.S, self.steps, self.B, self.H, self.topk, self.topk_idx, self.radius,
                                    [self.csr[k][0] for k in self.steps], [self.csr[k][1] for k in self.steps],
-                                   prev_dilation=self.dil)
+                                   prev_dilation=self.dil,
+                                   orders=[self.orders[k] for k in self.steps] if orders else None)
 
-    def attn_step(self, k, Q_all, K_all, V_all, lse=None, use_schedule=True):
+    def attn_step(self, k, Q_all, K_all, V_all, lse=None, use_schedule=True, use_order=False):
         rp, ci, sch = self.csr[k]
+        if use_order:
+            sch, use_schedule = self.orders[k], True
         sv.sparvar_block_sparse_attn_fwd(self.g, k, self.q_slice(Q_all, k), self.kv_prefix(K_all, k),
                                          self.kv_prefix(V_all, k), self.out[k], rp, ci, lse=lse,
                                          schedule=sch if use_schedule else None, softmax_scale=self.scale)

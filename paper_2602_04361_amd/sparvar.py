@@ -90,7 +90,8 @@ def load_library(path: str = LIB_PATH):
                                                     f32, vp, vp]),
         "sparvar_cs4a_select_tokens": (ctypes.c_int, [vp, i32, i32, i32, vp, vp]),
         "sparvar_cs4a_row_stride": (i32, [G, i32]),
-        "sparvar_map_index_steps": (ctypes.c_int, [G, i32, i32, vp, i32, i32, i32, vp, i32, i32, vp, vp, vp, vp]),
+        "sparvar_map_index_steps": (ctypes.c_int, [G, i32, i32, vp, i32, i32, i32, vp, i32, i32, vp, vp, vp, vp,
+                                                   vp]),
         "sparvar_kv_compact": (ctypes.c_int, [G, i32, vp, i32, i32, i32, ctypes.c_int, vp, vp, i64, vp, vp, i64, vp]),
         "sparvar_csla_row_stride": (i32, [G, i32, i32]),
         "sparvar_csla_block_rows": (ctypes.c_int, [G, i32, vp, i32, vp, i32, vp]),
@@ -362,8 +363,9 @@ def sparvar_map_index(geom, S, k, B, H, topk, topk_idx, local_row_ptr, local_col
 
 
 def sparvar_map_index_steps(geom, S, ks, B, H, topk, topk_idx, radius, row_ptrs, col_idxs, prev_dilation=0,
-                            stream=None):
-    """The rows of several target scales in one launch (local rows generated, no schedule)."""
+                            orders=None, stream=None):
+    """The rows of several target scales in one launch (local rows generated); with orders (one int32 tensor of
+    B*H*G_k entries, or None, per step) also the attention launch order of each step."""
     n = len(ks)
     if not (len(row_ptrs) == len(col_idxs) == n):
         raise SparvarError(ERR_INVALID, "one row_ptr and col_idx per step is required")
@@ -372,9 +374,15 @@ def sparvar_map_index_steps(geom, S, ks, B, H, topk, topk_idx, radius, row_ptrs,
     ci_arr = (ctypes.c_void_p * max(n, 1))(*[t.data_ptr() for t in col_idxs])
     cap_arr = (ctypes.c_int64 * max(n, 1))(*[t.numel() for t in col_idxs])
     vp = ctypes.c_void_p
+    ord_arr = None
+    if orders is not None:
+        if len(orders) != n:
+            raise SparvarError(ERR_INVALID, "one order (or None) per step is required")
+        ord_arr = (ctypes.c_void_p * max(n, 1))(*[(t.data_ptr() if t is not None else None) for t in orders])
     _check(load_library().sparvar_map_index_steps(geom.ref, S, n, ctypes.cast(k_arr, vp), B, H, topk,
                                                   _ptr(topk_idx), radius, prev_dilation, ctypes.cast(rp_arr, vp),
                                                   ctypes.cast(ci_arr, vp), ctypes.cast(cap_arr, vp),
+                                                  ctypes.cast(ord_arr, vp) if ord_arr is not None else None,
                                                   _stream(stream)))
 
 

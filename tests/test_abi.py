@@ -197,7 +197,8 @@ def test_map_steps_validation_before_launch():
         p_arr = (ctypes.c_void_p * 3)(rp, fake, fake)
         c_arr = (ctypes.c_int64 * 3)(*caps)
         return lib.sparvar_map_index_steps(g.ref, S, n, ctypes.cast(k_arr, vp), 2, 16, topk, vp(fake), 1, 0,
-                                           ctypes.cast(p_arr, vp), ctypes.cast(p_arr, vp), ctypes.cast(c_arr, vp), None)
+                                           ctypes.cast(p_arr, vp), ctypes.cast(p_arr, vp), ctypes.cast(c_arr, vp), None,
+                                           None)
     assert call(0, (11, 12, 13), cap) == sv.ERR_INVALID            # no step
     assert call(9, (11, 12, 13), cap) == sv.ERR_INVALID            # more than eight
     assert call(3, (11, 12, 10), cap) == sv.ERR_INVALID            # k <= S

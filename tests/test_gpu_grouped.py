@@ -109,3 +109,76 @@ def test_forms_on_pipeline_rows(monkeypatch, form):
         monkeypatch.setenv(key, val)
     run_case(INF_SIDES, INF_SIDES, 8, 4, 10, [11, 12, 13], 1, 4, 128, 32, 8, 1, "bf16", seed=12,
              tiles_per_step=16)
+
+
+def check_order(order, lengths, n_items, grouped, item_len):
+    """order: launch positions -> items (rows, or -2 - group); a permutation of the
+    items, each XCD share of positions holding its own items, longest first
+    (ties in item order)."""
+    per = -(-n_items // 8)
+    got = order[:n_items].tolist()
+    items = [(-2 - v) if grouped else v for v in got]
+    assert sorted(items) == list(range(n_items))
+    for x in range(8):
+        lo, hi = x * per, min((x + 1) * per, n_items)
+        share = items[lo:hi]
+        assert sorted(share) == list(range(lo, hi))
+        keys = [(-item_len(i), i) for i in share]
+        assert keys == sorted(keys)
+
+
+@pytest.mark.parametrize("form", ["per_tile", "group4"])
+def test_launch_order_from_the_mapping(monkeypatch, form):
+    # one mapping launch writes every step's order; the attention gives the same
+    # bits with and without it, and ignores an order of the other form
+    for key, val in FORMS[form].items():
+        monkeypatch.setenv(key, val)
+    from paper_2602_04361_amd.pipeline import SparsePath
+
+    h, b, ns, S, steps, B, H, d = INF_SIDES, 8, 4, 10, [11, 12, 13], 1, 4, 128
+    note(f"[order] form={form}")
+    q, kk, v = make_case(h, h, B, H, d, 8, ns, 70, "bf16")
+    Q, K, V = to_dev(q, "bf16"), to_dev(kk, "bf16"), to_dev(v, "bf16")
+    g = sv.Geometry(h, h, b, ns)
+    og = oracle_geometry(h, h, b, ns)
+    path = SparsePath(g, S, steps, B, H, d, 8, 1, use_schedule=True)
+    path.decision(Q, K, V)
+    path.map_all(orders=True)
+    torch.cuda.synchronize()
+    grouped = form != "per_tile"
+    for k in steps:
+        rp, ci, _ = path.csr[k]
+        ci_h = ci.cpu().numpy()
+        M = int(rp[1].item() - rp[0].item())
+        n_rows = B * H * og.tiles(k)
+        lens = [int((ci_h[r * M:(r + 1) * M] >= 0).sum()) for r in range(n_rows)]
+        Th, Tw = og.Th(k), og.Tw(k)
+        if grouped:
+            ngc, ngr = -(-Tw // 2), Th
+            n_items = B * H * ngr * ngc
+
+            def item_len(i):
+                bh, gi = divmod(i, ngr * ngc)
+                A, Cg = divmod(gi, ngc)
+                return sum(lens[bh * Th * Tw + A * Tw + c] for c in (2 * Cg, 2 * Cg + 1) if c < Tw)
+        else:
+            n_items = n_rows
+
+            def item_len(i):
+                return lens[i]
+        check_order(path.orders[k].cpu().numpy(), lens, n_items, grouped, item_len)
+        path.attn_step(k, Q, K, V, use_schedule=False)
+        torch.cuda.synchronize()
+        ref = path.out[k].clone()
+        path.out[k].zero_()
+        path.attn_step(k, Q, K, V, use_order=True)
+        torch.cuda.synchronize()
+        assert torch.equal(path.out[k], ref), f"step {k}: results depend on the launch order"
+        # the other kind of order is ignored: a row permutation for groups, a group order for tiles
+        other = torch.arange(n_rows, dtype=torch.int32, device="cuda").flip(0) if grouped else \
+            -2 - torch.arange(n_rows, dtype=torch.int32, device="cuda")
+        path.out[k].zero_()
+        sv.sparvar_block_sparse_attn_fwd(g, k, path.q_slice(Q, k), path.kv_prefix(K, k), path.kv_prefix(V, k),
+                                         path.out[k], rp, ci, schedule=other, softmax_scale=path.scale)
+        torch.cuda.synchronize()
+        assert torch.equal(path.out[k], ref), f"step {k}: an order of the other form changed the results"
