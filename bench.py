@@ -207,7 +207,7 @@ def sweep(args, dev):
         path = SparsePath(g, st["S"], st["steps"], B, H, d, st["topk"], st["radius"])
         info = path.info
         stream = torch.cuda.current_stream()
-        n_ev = 2 + 2 * len(st["steps"])
+        n_ev = 3 + len(st["steps"])
 
         def one(i, ev=None):
             Q, K, V = sets[i % len(sets)]
@@ -216,13 +216,13 @@ def sweep(args, dev):
             path.decision(Q, K, V)
             if ev is not None:
                 ev[1].record(stream)
+            path.map_all(orders=True)
+            if ev is not None:
+                ev[2].record(stream)
             for j, kk in enumerate(st["steps"]):
-                path.map_step(kk)
+                path.attn_step(kk, Q, K, V, use_order=True)
                 if ev is not None:
-                    ev[2 + 2 * j].record(stream)
-                path.attn_step(kk, Q, K, V)
-                if ev is not None:
-                    ev[3 + 2 * j].record(stream)
+                    ev[3 + j].record(stream)
 
         for i in range(5):
             one(i)
@@ -234,14 +234,14 @@ def sweep(args, dev):
         torch.cuda.synchronize()
         med = lambda a, b: float(np.median([evs[i][a].elapsed_time(evs[i][b]) for i in range(n)]))
         out = {"sweep": st["name"], "B": B, "H": H, "block": st["b"], "topk": st["topk"], "radius": st["radius"],
-               "decision_scale": st["sides"][st["S"] - 1], "decision_ms": med(0, 1), "steps": {}}
+               "decision_scale": st["sides"][st["S"] - 1], "decision_ms": med(0, 1),
+               "map_all_steps_ms": med(1, 2), "steps": {}}
         BH = B * H
         for j, kk in enumerate(st["steps"]):
             rp, ci, _ = path.csr[kk]
             f, b_, dens, _ = sparse_accounting(rp.cpu().numpy(), ci.cpu().numpy(), info, kk, BH, d)
-            t_attn = med(2 + 2 * j, 3 + 2 * j)
-            t_map = med(1 + 2 * j, 2 + 2 * j)
-            out["steps"][str(info[kk]["h"])] = {"map_ms": t_map, "attn_ms": t_attn, "gflop": f / 1e9,
+            t_attn = med(2 + j, 3 + j)
+            out["steps"][str(info[kk]["h"])] = {"attn_ms": t_attn, "gflop": f / 1e9,
                                                 "tflops": f / t_attn / 1e9,
                                                 "frac_bf16_peak": f / t_attn / 1e9 / PEAK_BF16_TFLOPS,
                                                 "density": dens}

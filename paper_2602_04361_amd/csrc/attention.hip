@@ -1617,11 +1617,15 @@ hipError_t launch_grouped(const SparseAttnArgs& a, int nw, int wpt, int kc, int 
 
 int group_waves_for(const GeoTable& G, int k, int32_t BH, int num_cu, int group_waves) {
   if (group_waves >= 0) return group_waves;
+  // Automatic choice. With the launch order of the mapping call (longest first
+  // inside each XCD's share), one tile per workgroup is the faster form up to
+  // about two rounds of workgroups (Infinity 64x64 step, 2048 tiles: 105 against
+  // 111 us for pairs of tiles); from 16 tiles per CU on (2048x2048 schedule,
+  // 128x128 step: 4096 tiles), pairs of 64-query tiles (quads of 32-query tiles)
+  // sharing each staged chunk are faster (285 against 307 us).
   const int wpt = waves_for(G.eh[k - 1] * G.ew[k - 1]);
   if (wpt > 2) return 0;
-  const int32_t gh = wpt == 2 ? 1 : 2, gw = 2;  // 1 x 2 or 2 x 2 tiles
-  const int64_t groups = (int64_t)BH * ((G.Th[k - 1] + gh - 1) / gh) * ((G.Tw[k - 1] + gw - 1) / gw);
-  return groups >= 4 * (int64_t)num_cu ? 4 : 0;
+  return (int64_t)BH * tiles_of(G, k) >= 16 * (int64_t)num_cu ? 4 : 0;
 }
 
 SparseForm sparse_form(const GeoTable& G, int k, int32_t BH, int num_cu, int group_waves) {
@@ -1644,11 +1648,9 @@ hipError_t launch_sparse_attn(const SparseAttnArgs& a, hipStream_t stream) {
   const int k = a.k;
   const int32_t tile_q = G.eh[k - 1] * G.ew[k - 1];
   const int wpt = waves_for(tile_q);
-  // grouped path: several query tiles per workgroup share each staged chunk.
-  // Automatic choice: pairs of 64-query tiles (or quads of 32-query tiles) in
-  // 4-wave workgroups, when that still gives every CU at least four workgroups;
-  // with fewer, the last round of workgroups runs the chip part-empty and one
-  // tile per workgroup is faster.
+  // grouped path: several query tiles per workgroup share each staged chunk
+  // (pairs of 64-query tiles or quads of 32-query tiles in 4-wave workgroups,
+  // or 8-wave groups), when group_waves asks for it.
   const int gwv = group_waves_for(G, k, a.BH, a.num_cu, a.group_waves);
   if (a.bf16 && a.waves <= 0 && gwv > wpt) {
     int kc = a.group_chunk, ns = a.group_stages;

@@ -196,10 +196,10 @@ hipError_t launch_local_blocks(const GeoTable& G, int k, int32_t radius, int32_t
 }
 
 // Launch order of the block-sparse kernel's work items (query tiles, or groups
-// of neighbouring tiles) at one step: inside each XCD's share of the launch
-// positions (the items the XCD-aware order gives that XCD), items go longest
-// first (length = the rows' entries, summed over a group's tiles; ties keep the
-// item order), so the workgroups that start last are the short ones.
+// of neighbouring tiles) at one step: inside each half of each XCD's share of
+// the launch positions (the items the XCD-aware order gives that XCD), items go
+// longest first (length = the rows' entries, summed over a group's tiles; ties
+// keep the item order), so the workgroups that start last are the short ones.
 struct OrderStep {
   int32_t* order;
   const int32_t* counts;
@@ -244,10 +244,15 @@ __global__ __launch_bounds__(kOrderThreads) void order_kernel(OrderIO io) {
     key[i] = len;
   }
   __syncthreads();
+  // two windows per share, ranked separately: the first half of the share's
+  // positions keeps the first half of its items (the XCD works on about as many
+  // (b, h) planes at a time as in natural order, so its L2 keeps their K/V)
+  const int32_t w = (n + 1) / 2;
   for (int32_t i = threadIdx.x; i < n; i += kOrderThreads) {
+    const int32_t w0 = i < w ? 0 : w, w1 = i < w ? w : n;
     const int32_t ki = key[i];
-    int32_t rank = 0;
-    for (int32_t j = 0; j < n; ++j) {
+    int32_t rank = w0;
+    for (int32_t j = w0; j < w1; ++j) {
       const int32_t kj = key[j];
       rank += (kj > ki) | ((kj == ki) & (j < i));
     }
