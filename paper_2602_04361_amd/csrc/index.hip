@@ -214,12 +214,22 @@ struct OrderIO {
 constexpr int kOrderThreads = 256;
 constexpr int kOrderMaxPer = 4096;
 
-// Grid (8 XCD shares, steps); one workgroup ranks one share.
+// Grid (8 XCD shares x 2 windows, steps); one workgroup ranks one window. The
+// two windows of a share are ranked separately: the first half of the share's
+// positions keeps the first half of its items (the XCD works on about as many
+// (b, h) planes at a time as in natural order, so its L2 keeps their K/V). The
+// split is rounded up to a multiple of 4.
 __global__ __launch_bounds__(kOrderThreads) void order_kernel(OrderIO io) {
-  __shared__ int32_t key[kOrderMaxPer];
+  __shared__ __attribute__((aligned(16))) int32_t key[kOrderMaxPer + 4];
   const OrderStep& s = io.st[blockIdx.y];
-  const int32_t lo = (int32_t)blockIdx.x * s.per;
-  const int32_t hi = lo + s.per < s.n_items ? lo + s.per : s.n_items;
+  const int32_t share = (int32_t)blockIdx.x >> 1, second = (int32_t)blockIdx.x & 1;
+  const int32_t s_lo = share * s.per;
+  const int32_t s_hi = s_lo + s.per < s.n_items ? s_lo + s.per : s.n_items;
+  const int32_t n_share = s_hi - s_lo;
+  if (n_share <= 0) return;
+  const int32_t half = (n_share + 1) / 2;
+  const int32_t w = ((half + 3) & ~3) < n_share ? ((half + 3) & ~3) : n_share;
+  const int32_t lo = s_lo + (second ? w : 0), hi = second ? s_hi : s_lo + w;
   const int32_t n = hi - lo;
   if (n <= 0) return;
   const bool grouped = s.gh > 0;
@@ -243,18 +253,19 @@ __global__ __launch_bounds__(kOrderThreads) void order_kernel(OrderIO io) {
     }
     key[i] = len;
   }
+  if (threadIdx.x < 4) key[n + threadIdx.x] = INT32_MIN;  // padding: never ahead of a real length
   __syncthreads();
-  // two windows per share, ranked separately: the first half of the share's
-  // positions keeps the first half of its items (the XCD works on about as many
-  // (b, h) planes at a time as in natural order, so its L2 keeps their K/V)
-  const int32_t w = (n + 1) / 2;
+  const int4* key4 = reinterpret_cast<const int4*>(key);
   for (int32_t i = threadIdx.x; i < n; i += kOrderThreads) {
-    const int32_t w0 = i < w ? 0 : w, w1 = i < w ? w : n;
     const int32_t ki = key[i];
-    int32_t rank = w0;
-    for (int32_t j = w0; j < w1; ++j) {
-      const int32_t kj = key[j];
-      rank += (kj > ki) | ((kj == ki) & (j < i));
+    int32_t rank = 0;
+    for (int32_t j4 = 0; j4 < (n + 3) >> 2; ++j4) {
+      const int4 kk = key4[j4];
+      const int32_t j = j4 << 2;
+      rank += (kk.x > ki) | ((kk.x == ki) & (j < i));
+      rank += (kk.y > ki) | ((kk.y == ki) & (j + 1 < i));
+      rank += (kk.z > ki) | ((kk.z == ki) & (j + 2 < i));
+      rank += (kk.w > ki) | ((kk.w == ki) & (j + 3 < i));
     }
     s.order[lo + rank] = grouped ? -2 - (lo + i) : lo + i;
   }
@@ -283,7 +294,7 @@ hipError_t launch_map_order(const GeoTable& G, int32_t BH, int32_t topk, int n_s
     if (o.order) ++used;
   }
   if (used == 0) return hipSuccess;
-  hipLaunchKernelGGL(order_kernel, dim3(8, n_steps), dim3(kOrderThreads), 0, stream, io);
+  hipLaunchKernelGGL(order_kernel, dim3(16, n_steps), dim3(kOrderThreads), 0, stream, io);
   return hipGetLastError();
 }
 

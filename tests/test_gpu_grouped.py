@@ -113,18 +113,23 @@ def test_forms_on_pipeline_rows(monkeypatch, form):
 
 def check_order(order, lengths, n_items, grouped, item_len):
     """order: launch positions -> items (rows, or -2 - group); a permutation of the
-    items, each XCD share of positions holding its own items, longest first
-    (ties in item order)."""
+    items, each half of each XCD share of positions holding its own items,
+    longest first (ties in item order)."""
     per = -(-n_items // 8)
     got = order[:n_items].tolist()
     items = [(-2 - v) if grouped else v for v in got]
     assert sorted(items) == list(range(n_items))
     for x in range(8):
         lo, hi = x * per, min((x + 1) * per, n_items)
-        share = items[lo:hi]
-        assert sorted(share) == list(range(lo, hi))
-        keys = [(-item_len(i), i) for i in share]
-        assert keys == sorted(keys)
+        if hi <= lo:
+            continue
+        n = hi - lo
+        w = min(((n + 1) // 2 + 3) & ~3, n)
+        for a, b in ((lo, lo + w), (lo + w, hi)):
+            window = items[a:b]
+            assert sorted(window) == list(range(a, b))
+            keys = [(-item_len(i), i) for i in window]
+            assert keys == sorted(keys)
 
 
 @pytest.mark.parametrize("form", ["per_tile", "group4"])
