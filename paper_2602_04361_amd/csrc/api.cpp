@@ -340,6 +340,7 @@ int sparvar_cs4a_column_sums(const sparvar_geometry_t* g, int32_t S, int32_t C, 
   a.k_bh_stride = k_bh_stride;
   a.softmax_scale = softmax_scale;
   a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
+  a.num_cu = device_cus();
   return hip_status(launch_cs4a_colsum(a, stream), "column-sum launch");
 }
 

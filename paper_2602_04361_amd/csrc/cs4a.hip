@@ -15,9 +15,13 @@
 namespace sparvar {
 
 // ---------------------------------------------------------------- column sums
-// One workgroup per (b, h, query block): NW = C / 32 waves of 32 queries. Keys
-// stream through LDS in 64-key chunks (direct loads, two stages in separate
-// arrays). Each wave computes S = Q K^T with MFMA (A = Q rows from registers,
+// One workgroup per (b, h, key range, query block): NW = C / 32 waves of 32
+// queries. The key axis is cut into n_splits ranges of whole chunks; the column
+// sums of different keys are independent, so the ranges need no reduction
+// between workgroups and only add parallelism (a plane has few query blocks).
+// Work items run (b, h)-major, then key range, then query block, so the
+// workgroups that share a range's K on one XCD run together. Keys stream through
+// LDS in 64-key chunks (direct loads, two stages in separate arrays). Each wave computes S = Q K^T with MFMA (A = Q rows from registers,
 // B = K rows from LDS), so a lane's accumulator column is one key and its 16
 // registers are 16 of the wave's queries: P = exp2(s * scale * log2e - LSE *
 // log2e), the sum over the registers and one half-wave exchange give the key's
@@ -29,6 +33,7 @@ struct ColsumIO {
   float* out;  // [planes, n_blocks, n_kv]
   int64_t q_bh_stride, k_bh_stride;
   int32_t n_q, n_kv, C, n_blocks, n_items, swizzle;
+  int32_t n_splits, split_chunks;  // key ranges, chunks per range
   float scale_log2;
 };
 
@@ -39,15 +44,17 @@ __global__ __launch_bounds__(NW * 64) void cs4a_colsum_kernel(ColsumIO io) {
   static_assert((KC * U) % NT == 0, "chunk must split evenly over the workgroup");
   __shared__ __attribute__((aligned(16))) char ks0[kTile];
   __shared__ __attribute__((aligned(16))) char ks1[kTile];
-  __shared__ float red[NW * KC];
+  __shared__ float red[2][NW * KC];  // per-wave sums of a chunk, by chunk parity
 
   const int32_t item = swizzled_item(blockIdx.x, gridDim.x, io.swizzle);
   if (item >= io.n_items) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, half = lane >> 5;
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);
-  const int32_t bh = item / io.n_blocks;
-  const int32_t g = item - bh * io.n_blocks;
+  const int32_t per_bh = io.n_splits * io.n_blocks;
+  const int32_t bh = item / per_bh;
+  const int32_t split = (item - bh * per_bh) / io.n_blocks;
+  const int32_t g = item - bh * per_bh - split * io.n_blocks;
   const int32_t q_end = (g + 1) * io.C < io.n_q ? (g + 1) * io.C : io.n_q;
   const int32_t q_first = g * io.C + wave * kQPerWave;
 
@@ -89,16 +96,31 @@ __global__ __launch_bounds__(NW * 64) void cs4a_colsum_kernel(ColsumIO io) {
       dma16(kbytes + (uint32_t)(tok * D + 8 * ld_unit[j]) * 2u, stg + first * 16);
     }
   };
-  float* orow = io.out + (int64_t)item * n_kv;
-  const int32_t n_chunks = (n_kv + KC - 1) / KC;
-  if (n_chunks > 0) issue(0, ks0);
+  float* orow = io.out + ((int64_t)bh * io.n_blocks + g) * n_kv;
+  const int32_t all_chunks = (n_kv + KC - 1) / KC;
+  const int32_t c_begin = split * io.split_chunks;
+  const int32_t c_end = c_begin + io.split_chunks < all_chunks ? c_begin + io.split_chunks : all_chunks;
+  // the sums of chunk c - 1 are reduced after the barrier of step c (their LDS
+  // row alternates with the chunk's parity), so a step has one barrier
+  auto reduce = [&](int32_t c) {
+    if (tid < KC) {
+      const float* rr = red[c & 1];
+      float t = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) t += rr[w * KC + tid];
+      const int32_t key = c * KC + tid;
+      if (key < n_kv) orow[key] = t;
+    }
+  };
+  if (c_begin < c_end) issue(c_begin * KC, ks0);
   auto step = [&](int32_t c, auto st_c) {
     constexpr int ST = decltype(st_c)::value;
     char* const stg = ST == 0 ? ks0 : ks1;
     char* const nstg = ST == 0 ? ks1 : ks0;
     __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __syncthreads();
-    if (c + 1 < n_chunks) issue((c + 1) * KC, nstg);
+    if (c + 1 < c_end) issue((c + 1) * KC, nstg);
+    if (c > c_begin) reduce(c - 1);
     f32x16 st[2];
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt) st[kt] = zero16();
@@ -116,20 +138,16 @@ __global__ __launch_bounds__(NW * 64) void cs4a_colsum_kernel(ColsumIO io) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) cs += __builtin_amdgcn_exp2f(__builtin_fmaf(st[kt][r], io.scale_log2, -lse2[r]));
       cs = sum_halves(cs);
-      if (half == 0) red[wave * KC + 32 * kt + l32] = cs;
-    }
-    __syncthreads();
-    if (tid < KC) {
-      float t = 0.f;
-#pragma unroll
-      for (int w = 0; w < NW; ++w) t += red[w * KC + tid];
-      const int32_t key = c * KC + tid;
-      if (key < n_kv) orow[key] = t;
+      if (half == 0) red[c & 1][wave * KC + 32 * kt + l32] = cs;
     }
   };
-  for (int32_t c = 0; c < n_chunks; c += 2) {
+  for (int32_t c = c_begin; c < c_end; c += 2) {
     step(c, std::integral_constant<int, 0>{});
-    if (c + 1 < n_chunks) step(c + 1, std::integral_constant<int, 1>{});
+    if (c + 1 < c_end) step(c + 1, std::integral_constant<int, 1>{});
+  }
+  if (c_begin < c_end) {
+    __syncthreads();
+    reduce(c_end - 1);
   }
 }
 
@@ -284,7 +302,15 @@ hipError_t launch_cs4a_colsum(const Cs4aColsumArgs& a, hipStream_t stream) {
   io.n_kv = a.n_kv;
   io.C = a.C;
   io.n_blocks = (a.n_q + a.C - 1) / a.C;
-  io.n_items = a.BH * io.n_blocks;
+  // key ranges: enough workgroups for about four per CU, at least 8 chunks each
+  const int32_t all_chunks = (a.n_kv + 63) / 64;
+  const int64_t base = (int64_t)a.BH * io.n_blocks;
+  const int64_t want = base > 0 ? (4 * (int64_t)(a.num_cu > 0 ? a.num_cu : 256) + base - 1) / base : 1;
+  int32_t splits = (int32_t)(want < all_chunks / 8 ? want : all_chunks / 8);
+  splits = splits < 1 ? 1 : splits;
+  io.split_chunks = (all_chunks + splits - 1) / splits;
+  io.n_splits = all_chunks > 0 ? (all_chunks + io.split_chunks - 1) / io.split_chunks : 1;
+  io.n_items = (int32_t)(base * io.n_splits);
   io.swizzle = a.swizzle;
   io.scale_log2 = a.softmax_scale * kLog2e;
   const int nw = a.C / kQPerWave;

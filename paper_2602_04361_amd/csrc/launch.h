@@ -77,6 +77,7 @@ struct Cs4aColsumArgs {
   int64_t q_bh_stride, k_bh_stride;
   float softmax_scale;
   int swizzle;
+  int num_cu;  // compute units of the device (key-range split)
 };
 
 struct TokenAttnArgs {
