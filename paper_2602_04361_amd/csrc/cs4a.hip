@@ -163,10 +163,15 @@ __device__ __forceinline__ uint32_t order_key(float f) {
 }
 
 constexpr int kTopkThreads = 256;
+constexpr int32_t kTopkStageMax = 8192;  // rows up to this length are staged in LDS (32 KB)
 
+// STAGED: the row's order keys are read from global memory once into LDS
+// (dynamic, n words); otherwise every pass reads them from global memory.
+template <bool STAGED>
 __global__ __launch_bounds__(kTopkThreads) void cs4a_topk_kernel(const float* __restrict__ in, int32_t n, int32_t K,
                                                                   int32_t* __restrict__ out) {
   constexpr int NT = kTopkThreads;
+  extern __shared__ uint32_t staged[];
   __shared__ int32_t hist[256];
   __shared__ int32_t wt[NT / 64];
   __shared__ uint32_t sel_prefix;
@@ -176,6 +181,13 @@ __global__ __launch_bounds__(kTopkThreads) void cs4a_topk_kernel(const float* __
   const float* x = in + row * n;
   int32_t* o = out + row * K;
   const int32_t nsel = K < n ? K : n;
+  if constexpr (STAGED) {
+    for (int32_t i = tid; i < n; i += NT) staged[i] = order_key(x[i]);
+  }
+  auto key = [&](int32_t i) -> uint32_t {
+    if constexpr (STAGED) return staged[i];
+    else return order_key(x[i]);
+  };
   uint32_t prefix = 0, mask = 0;
   int32_t remaining = nsel;
   if (K < n) {
@@ -183,7 +195,7 @@ __global__ __launch_bounds__(kTopkThreads) void cs4a_topk_kernel(const float* __
       hist[tid] = 0;  // NT == 256 bins
       __syncthreads();
       for (int32_t i = tid; i < n; i += NT) {
-        const uint32_t u = order_key(x[i]);
+        const uint32_t u = key(i);
         if ((u & mask) == prefix) atomicAdd(&hist[(u >> shift) & 255], 1);
       }
       __syncthreads();
@@ -202,22 +214,40 @@ __global__ __launch_bounds__(kTopkThreads) void cs4a_topk_kernel(const float* __
       __syncthreads();
     }
   }
-  // prefix: the K-th largest key; remaining: how many keys equal to it to keep
+  // prefix: the K-th largest key; remaining: how many keys equal to it to keep.
+  // Thread t owns the contiguous indices [t seg, (t + 1) seg): one scan ranks the
+  // keys equal to the threshold in index order, a second places the kept ones.
   const bool all = K >= n;
-  int32_t eq_before = 0, kept_before = 0;
-  for (int32_t base = 0; base < n; base += NT) {
-    const int32_t i = base + tid;
-    uint32_t u = 0;
-    if (i < n) u = order_key(x[i]);
-    const int32_t eq = (!all && i < n && u == prefix) ? 1 : 0;
-    int32_t eq_total;
-    const int32_t eq_rank = eq_before + block_excl_scan<NT>(eq, wt, eq_total);
-    const int32_t keep = (i < n) && (all || u > prefix || (eq && eq_rank < remaining)) ? 1 : 0;
-    int32_t keep_total;
-    const int32_t pos = kept_before + block_excl_scan<NT>(keep, wt, keep_total);
-    if (keep && pos < K) o[pos] = i;
-    eq_before += eq_total;
-    kept_before += keep_total;
+  const int32_t seg = (n + NT - 1) / NT;
+  const int32_t i0 = tid * seg, i1 = i0 + seg < n ? i0 + seg : n;
+  int32_t n_eq = 0;
+  if (!all)
+    for (int32_t i = i0; i < i1; ++i) n_eq += key(i) == prefix ? 1 : 0;
+  int32_t eq_total;
+  const int32_t eq_before = block_excl_scan<NT>(n_eq, wt, eq_total);
+  int32_t n_keep = 0;
+  {
+    int32_t e = eq_before;
+    for (int32_t i = i0; i < i1; ++i) {
+      const uint32_t u = key(i);
+      const bool eq = !all && u == prefix;
+      n_keep += (all || u > prefix || (eq && e < remaining)) ? 1 : 0;
+      e += eq ? 1 : 0;
+    }
+  }
+  int32_t keep_total;
+  int32_t pos = block_excl_scan<NT>(n_keep, wt, keep_total);
+  {
+    int32_t e = eq_before;
+    for (int32_t i = i0; i < i1; ++i) {
+      const uint32_t u = key(i);
+      const bool eq = !all && u == prefix;
+      if (all || u > prefix || (eq && e < remaining)) {
+        if (pos < K) o[pos] = i;
+        ++pos;
+      }
+      e += eq ? 1 : 0;
+    }
   }
   for (int32_t p = nsel + tid; p < K; p += NT) o[p] = -1;
 }
@@ -251,9 +281,18 @@ __device__ __forceinline__ int32_t map_token(const GeoTable& G, int32_t j, int S
 __global__ __launch_bounds__(kMapThreads) void cs4a_map_kernel(MapTokIO io) {
   constexpr int NT = kMapThreads;
   __shared__ int32_t wt[NT / 64];
+  // the geometry table in LDS: map_token indexes it per lane (scale search),
+  // which on the kernel-argument copy is a chain of dependent global loads
+  __shared__ GeoTable s_geo;
   const int32_t r = blockIdx.x;
   if (r >= io.rows) return;
   const int tid = threadIdx.x;
+  {
+    const int32_t* src = reinterpret_cast<const int32_t*>(&io.G);
+    int32_t* dst = reinterpret_cast<int32_t*>(&s_geo);
+    for (int i = tid; i < (int)(sizeof(GeoTable) / 4); i += NT) dst[i] = src[i];
+  }
+  __syncthreads();
   const int32_t bh = r / io.G_k;
   const int32_t g = r - bh * io.G_k;
   const int32_t src = (int32_t)(((int64_t)(2 * g + 1) * io.G_S) / (2 * (int64_t)io.G_k));
@@ -267,7 +306,7 @@ __global__ __launch_bounds__(kMapThreads) void cs4a_map_kernel(MapTokIO io) {
     const int32_t i = base + tid;
     const int32_t j = i < io.K ? in[i] : -1;
     int32_t m = -1;
-    if (j >= 0 && j < n_le_S) m = map_token(io.G, j, io.S, io.k);
+    if (j >= 0 && j < n_le_S) m = map_token(s_geo, j, io.S, io.k);
     const int32_t keep = m >= ns ? 1 : 0;
     int32_t total;
     const int32_t before = block_excl_scan<NT>(keep, wt, total);
@@ -323,7 +362,10 @@ hipError_t launch_cs4a_colsum(const Cs4aColsumArgs& a, hipStream_t stream) {
 
 hipError_t launch_cs4a_topk(const float* in, int32_t rows, int32_t n, int32_t K, int32_t* out, hipStream_t stream) {
   if (rows == 0) return hipSuccess;
-  hipLaunchKernelGGL(cs4a_topk_kernel, dim3(rows), dim3(kTopkThreads), 0, stream, in, n, K, out);
+  if (n <= kTopkStageMax)
+    hipLaunchKernelGGL(cs4a_topk_kernel<true>, dim3(rows), dim3(kTopkThreads), (size_t)n * 4, stream, in, n, K, out);
+  else
+    hipLaunchKernelGGL(cs4a_topk_kernel<false>, dim3(rows), dim3(kTopkThreads), 0, stream, in, n, K, out);
   return hipGetLastError();
 }
 

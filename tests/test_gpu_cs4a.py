@@ -98,7 +98,8 @@ def test_blocks_of_256_ragged_last_block():
 def test_select_tokens_ties_and_rows():
     # integer-valued rows with many ties, several row lengths around the radix passes
     r = np.random.default_rng(45)
-    for n, K in [(1, 1), (7, 3), (300, 257), (2521, 256), (4096, 1000)]:
+    # 9000 > 8192: the row is read from global memory on every pass instead of LDS
+    for n, K in [(1, 1), (7, 3), (300, 257), (2521, 256), (4096, 1000), (9000, 700), (9000, 9000)]:
         vals = r.integers(0, 6, size=(5, n)).astype(np.float32)
         vals[0] = -vals[0]  # negative values order correctly too
         d_vals = torch.from_numpy(vals).cuda()
