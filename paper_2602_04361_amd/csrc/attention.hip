@@ -928,7 +928,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
       const int r = ld_row[j];
       int32_t tok;
       if constexpr (Src::kTokens) tok = src.tokens[c.base + (r < c.count ? r : 0)];
-      else tok = chunk_token(c, r < c.count ? r : 0);
+      else tok = chunk_token(c, chunk_slot(r, c.count));
       const uint32_t off = (uint32_t)(tok * D + 8 * ld_unit[j]) * 2u;
       dma16(kbytes + off, kb + first * 16);
       dma16(vbytes + off, kb + kTile + first * 16);
@@ -1160,7 +1160,7 @@ __global__ __launch_bounds__(NW * 64) void attn_f32_kernel(AttnIO io, Src src) {
       const int gi = tid + j * NT;
       if (gi < kGroups) {
         const int slot = gi / (D / 4), c4 = gi % (D / 4);
-        const int32_t tok = chunk_token(c, slot < c.count ? slot : 0);
+        const int32_t tok = chunk_token(c, chunk_slot(slot, c.count));
         vreg[j] = ldg16(vplane + (int64_t)tok * D + 4 * c4);
       }
     }

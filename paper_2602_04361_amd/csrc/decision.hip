@@ -131,7 +131,7 @@ __global__ __launch_bounds__(WPT * KS * 64) void decision_kernel(DecisionIO io) 
       for (int j = 0; j < kLoads; ++j) {
         const int first = (j * WPT + slab) * 64;
         const int r = ld_row[j];
-        const uint32_t off = (uint32_t)(chunk_token(c, r < c.count ? r : 0) * D + 8 * ld_unit[j]) * 2u;
+        const uint32_t off = (uint32_t)(chunk_token(c, chunk_slot(r, c.count)) * D + 8 * ld_unit[j]) * 2u;
         dma16(kbytes + off, stg + first * 16);
         dma16(vbytes + off, stg + kTile + first * 16);
       }

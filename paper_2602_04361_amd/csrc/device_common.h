@@ -35,10 +35,17 @@ struct Chunk {
   uint32_t mask;
 };
 
+// Both products use the 24-bit multiplier, which issues at full rate where a
+// 32-bit integer multiply issues at quarter rate; every factor fits in 24 bits
+// (s < 64, magic <= 65536, 0 <= stride - nc < 65536).
 __device__ __forceinline__ int32_t chunk_token(const Chunk& c, int32_t s) {
-  const int32_t q = (s * c.magic) >> 16;
-  return c.base + q * c.stride + (s - q * c.nc);
+  const uint32_t q = __umul24((uint32_t)s, (uint32_t)c.magic) >> 16;
+  return c.base + s + (int32_t)__umul24(q, (uint32_t)(c.stride - c.nc));
 }
+
+// Slot a copying lane reads: slots past the chunk's count read its first key
+// (their scores are masked), so every lane issues the same copies.
+__device__ __forceinline__ int32_t chunk_slot(int32_t s, int32_t count) { return s < count ? s : 0; }
 
 // ceil(65536 / n) for n = 0..64 (entry 0 unused).
 __constant__ const uint32_t kNcMagic[65] = {
@@ -155,7 +162,7 @@ __device__ __forceinline__ void chunk_scores(const bf16_bits* kplane, const Chun
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt) {
     const int32_t s = 32 * kt + l32;
-    krow[kt] = kplane + (int64_t)chunk_token(c, s < c.count ? s : 0) * D + 8 * half;
+    krow[kt] = kplane + (int64_t)chunk_token(c, chunk_slot(s, c.count)) * D + 8 * half;
     st[kt] = zero16();
   }
 #pragma unroll
@@ -173,7 +180,7 @@ __device__ __forceinline__ void chunk_scores(const float* kplane, const Chunk& c
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt) {
     const int32_t s = 32 * kt + l32;
-    krow[kt] = kplane + (int64_t)chunk_token(c, s < c.count ? s : 0) * D + half;
+    krow[kt] = kplane + (int64_t)chunk_token(c, chunk_slot(s, c.count)) * D + half;
     st[kt] = zero16();
   }
 #pragma unroll

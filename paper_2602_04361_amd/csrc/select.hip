@@ -156,7 +156,7 @@ __global__ __launch_bounds__(WPT * TPW * 64) void pooled_scores_kernel(ScoreIO i
     for (int j = 0; j < kLoads; ++j) {
       const int first = (j * NW + wave_s) * 64;
       const int r = ld_row[j];
-      const uint32_t off = (uint32_t)(chunk_token(c, r < c.count ? r : 0) * D + 8 * ld_unit[j]) * 2u;
+      const uint32_t off = (uint32_t)(chunk_token(c, chunk_slot(r, c.count)) * D + 8 * ld_unit[j]) * 2u;
       dma16(kbytes + off, (SG == 0 ? kstage0 : kstage1) + first * 16);
     }
   };
