@@ -42,6 +42,15 @@
  *
  * Return value: SPARVAR_OK (0) or a negative status; a message for the last
  * failure on the calling thread is available from sparvar_last_error().
+ *
+ * Launch shapes are chosen automatically. For measurements, environment
+ * variables read at each call override them: SPARVAR_DENSE_WAVES / _CHUNK /
+ * _STAGES (dense attention), SPARVAR_SPARSE_WAVES / _CHUNK / _STAGES and
+ * SPARVAR_SPARSE_GROUP_WAVES / _GROUP_CHUNK / _GROUP_STAGES (block-sparse
+ * attention; group waves 0 = one query tile per workgroup), SPARVAR_CSLA_CHUNK
+ * / _STAGES, SPARVAR_DECISION_FUSED and SPARVAR_SWIZZLE (0 = natural workgroup
+ * order). A shape that is not built falls back to the default; results do not
+ * depend on the shape beyond floating-point summation order.
  */
 #ifndef SPARVAR_H_
 #define SPARVAR_H_
