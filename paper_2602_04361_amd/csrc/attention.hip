@@ -992,12 +992,36 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
     f32x16 st[KC / 32];
 #pragma unroll
     for (int kt = 0; kt < KC / 32; ++kt) st[kt] = zero16();
+    // Sparse sources with 32-key chunks read the whole K chunk first and issue the
+    // V^T reads under the S^T products, so no read waits behind a product (left
+    // to itself the compiler pairs each two reads with a full wait). The other
+    // shapes keep the compiler's order: the extra registers would cost them a
+    // wave per SIMD.
+    constexpr bool kHoist = KC == 32 && Src::kSparse;
+    i16x4 vlo[KC / 16][D / 32], vhi[KC / 16][D / 32];
+    if constexpr (kHoist) {
+      u32x4 kf[D / 16];
 #pragma unroll
-    for (int s2 = 0; s2 < D / 16; ++s2) {
+      for (int s2 = 0; s2 < D / 16; ++s2) kf[s2] = *reinterpret_cast<const u32x4*>(kst + k_off[0][s2]);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int kt = 0; kt < KC / 32; ++kt) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(kst + k_off[kt][s2]);
-        st[kt] = mfma_bf16(as_bf16x8(a), qf.f[s2], st[kt]);
+      for (int s2 = 0; s2 < D / 16; ++s2) st[0] = mfma_bf16(as_bf16x8(kf[s2]), qf.f[s2], st[0]);
+#pragma unroll
+      for (int ks = 0; ks < KC / 16; ++ks)
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt) {
+          vlo[ks][dt] = lds_read_tr(kst + v_off[0][dt] + ks * 16 * kRow);
+          vhi[ks][dt] = lds_read_tr(kst + v_off[1][dt] + ks * 16 * kRow);
+        }
+      __builtin_amdgcn_sched_barrier(0);
+    } else {
+#pragma unroll
+      for (int s2 = 0; s2 < D / 16; ++s2) {
+#pragma unroll
+        for (int kt = 0; kt < KC / 32; ++kt) {
+          const u32x4 a = *reinterpret_cast<const u32x4*>(kst + k_off[kt][s2]);
+          st[kt] = mfma_bf16(as_bf16x8(a), qf.f[s2], st[kt]);
+        }
       }
     }
 
@@ -1045,8 +1069,14 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
       const bf16x8 pf = as_bf16x8(w);
 #pragma unroll
       for (int dt = 0; dt < D / 32; ++dt) {
-        const i16x4 lo = lds_read_tr(kst + v_off[0][dt] + ks * 16 * kRow);
-        const i16x4 hi = lds_read_tr(kst + v_off[1][dt] + ks * 16 * kRow);
+        i16x4 lo, hi;
+        if constexpr (kHoist) {
+          lo = vlo[ks][dt];
+          hi = vhi[ks][dt];
+        } else {
+          lo = lds_read_tr(kst + v_off[0][dt] + ks * 16 * kRow);
+          hi = lds_read_tr(kst + v_off[1][dt] + ks * 16 * kRow);
+        }
         u32x4 av;
         av[0] = __builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 0, 1));
         av[1] = __builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 2, 3));
