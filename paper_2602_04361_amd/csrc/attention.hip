@@ -980,29 +980,35 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
     }
     __syncthreads();
     const Chunk c = ring[0];
+    const char* kst = SV_STAGE(S);
+    // waves of a grouped launch skip chunks their query tile does not list
+    const bool active = !Src::kGrouped || ((c.mask >> my_tile) & 1u);
+    // Sparse sources with 32-key chunks read the whole K chunk first, then look up
+    // and copy the next chunk while those reads land, and issue the V^T reads
+    // under the S^T products: no read waits behind a product or behind the next
+    // chunk's descriptor (left to itself the compiler pairs each two K reads with a
+    // full wait, after the descriptor lookup). The other shapes keep the
+    // compiler's order: the extra registers would cost them a wave per SIMD.
+    constexpr bool kHoist = KC == 32 && Src::kSparse;
+    u32x4 kf[D / 16];
+    if constexpr (kHoist) {
+      if (active) {
+#pragma unroll
+        for (int s2 = 0; s2 < D / 16; ++s2) kf[s2] = *reinterpret_cast<const u32x4*>(kst + k_off[0][s2]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
     Chunk cn;
     const bool have_n = ahead == NS - 2 && cur.next(cn);
     if (have_n) issue(cn, std::integral_constant<int, (S + NS - 1) % NS>{});
 
-    const char* kst = SV_STAGE(S);
-    // waves of a grouped launch skip chunks their query tile does not list
-    const bool active = !Src::kGrouped || ((c.mask >> my_tile) & 1u);
     if (active) {
     // ---- S^T = K Q^T
     f32x16 st[KC / 32];
 #pragma unroll
     for (int kt = 0; kt < KC / 32; ++kt) st[kt] = zero16();
-    // Sparse sources with 32-key chunks read the whole K chunk first and issue the
-    // V^T reads under the S^T products, so no read waits behind a product (left
-    // to itself the compiler pairs each two reads with a full wait). The other
-    // shapes keep the compiler's order: the extra registers would cost them a
-    // wave per SIMD.
-    constexpr bool kHoist = KC == 32 && Src::kSparse;
     i16x4 vlo[KC / 16][D / 32], vhi[KC / 16][D / 32];
     if constexpr (kHoist) {
-      u32x4 kf[D / 16];
-#pragma unroll
-      for (int s2 = 0; s2 < D / 16; ++s2) kf[s2] = *reinterpret_cast<const u32x4*>(kst + k_off[0][s2]);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int s2 = 0; s2 < D / 16; ++s2) st[0] = mfma_bf16(as_bf16x8(kf[s2]), qf.f[s2], st[0]);
