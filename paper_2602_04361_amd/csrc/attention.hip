@@ -1506,12 +1506,13 @@ hipError_t launch_block_row_attn(const BlockRowAttnArgs& a, hipStream_t stream) 
     return s;
   };
   int kc = a.chunk, ns = a.stages;
-  if (!(a.d == 128 && nw >= 2 && kc == 32 && (ns == 3 || ns == 4))) kc = 64, ns = 2;
+  if (!(a.d == 128 && nw >= 2 && kc == 32 && ns >= 2 && ns <= 4)) kc = 64, ns = 2;
 #define SV_BLK(DD, NN, KK, SS) \
   if (a.d == DD && nw == NN && kc == KK && ns == SS) \
     return launch_bf16<DD, NN, KK, SS>(io, make(BlockRowSrc<KK>{}), stream);
 #define SV_BLK2(DD, NN, KK) SV_BLK(DD, NN, KK, 2)
   SV_TOKEN_SHAPES(SV_BLK2)
+  SV_BLK(128, 2, 32, 2) SV_BLK(128, 4, 32, 2) SV_BLK(128, 8, 32, 2)
   SV_BLK(128, 2, 32, 3) SV_BLK(128, 4, 32, 3) SV_BLK(128, 8, 32, 3)
   SV_BLK(128, 2, 32, 4) SV_BLK(128, 4, 32, 4) SV_BLK(128, 8, 32, 4)
 #undef SV_BLK2

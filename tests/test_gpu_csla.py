@@ -131,7 +131,7 @@ def test_attention_empty_rows_give_zero_and_stop_at_first_invalid_id():
     assert_close(got, ref, "bf16", "rows cut at the first invalid id")
 
 
-@pytest.mark.parametrize("stages", [3, 4])
+@pytest.mark.parametrize("stages", [2, 3, 4])
 def test_attention_chunks_of_32(monkeypatch, stages):
     # the 32-key chunk shapes (d = 128, two to eight waves)
     monkeypatch.setenv("SPARVAR_CSLA_CHUNK", "32")
