@@ -48,9 +48,10 @@
  * _STAGES (dense attention), SPARVAR_SPARSE_WAVES / _CHUNK / _STAGES and
  * SPARVAR_SPARSE_GROUP_WAVES / _GROUP_CHUNK / _GROUP_STAGES (block-sparse
  * attention; group waves 0 = one query tile per workgroup), SPARVAR_CSLA_CHUNK
- * / _STAGES, SPARVAR_DECISION_FUSED and SPARVAR_SWIZZLE (0 = natural workgroup
- * order). A shape that is not built falls back to the default; results do not
- * depend on the shape beyond floating-point summation order.
+ * / _STAGES, SPARVAR_CS4A_CHUNK (token gather attention), SPARVAR_DECISION_FUSED
+ * and SPARVAR_SWIZZLE (0 = natural workgroup order). A shape that is not built
+ * falls back to the default; results do not depend on the shape beyond
+ * floating-point summation order.
  */
 #ifndef SPARVAR_H_
 #define SPARVAR_H_

@@ -435,6 +435,8 @@ int sparvar_cs4a_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t C, int
   a.epi_mode = mode;
   a.epi_base = mode == 0 ? nullptr : base;
   a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
+  a.chunk = env_int("SPARVAR_CS4A_CHUNK", -1);
+  a.num_cu = device_cus();
   return hip_status(launch_token_attn(a, stream), "token attention launch");
 }
 

@@ -1474,8 +1474,20 @@ hipError_t launch_token_attn(const TokenAttnArgs& a, hipStream_t stream) {
     return s;
   };
 #define SV_TOK(DD, NN, KK) \
-  if (a.d == DD && nw == NN) return launch_bf16<DD, NN, KK, 2>(io, make(TokenSrc<KK>{}), stream);
+  if (a.d == DD && nw == NN && kc == KK) return launch_bf16<DD, NN, KK, 2>(io, make(TokenSrc<KK>{}), stream);
+  // 32-key chunks (d = 128) halve the LDS of a workgroup: four 2-wave workgroups
+  // per CU instead of two, three 4-wave ones instead of two. Automatic choice:
+  // always for 2 waves, for 4 waves when it takes fewer rounds of workgroups.
+  int kc = 64;
+  if (a.d == 128 && nw >= 2 && nw <= 4) {
+    const int64_t r64 = (io.n_items + 2LL * a.num_cu - 1) / (2LL * a.num_cu);
+    const int64_t r32 = (io.n_items + (nw == 2 ? 4LL : 3LL) * a.num_cu - 1) / ((nw == 2 ? 4LL : 3LL) * a.num_cu);
+    if (a.chunk == 32 || (a.chunk < 0 && (nw == 2 || r32 < r64))) kc = 32;
+  } else if (a.d == 128 && nw == 8 && a.chunk == 32) {
+    kc = 32;
+  }
   SV_TOKEN_SHAPES(SV_TOK)
+  SV_TOK(128, 2, 32) SV_TOK(128, 4, 32) SV_TOK(128, 8, 32)
 #undef SV_TOK
   return hipErrorInvalidValue;
 }

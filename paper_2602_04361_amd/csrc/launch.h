@@ -92,6 +92,8 @@ struct TokenAttnArgs {
   const void* epi_base;
   int32_t up_hs, up_ws, up_hk, up_wk;
   int swizzle;
+  int chunk = -1;  // keys per chunk: 32 or 64 (32 only for d = 128), < 0 = automatic
+  int num_cu = 256;
 };
 
 // 1-D key blocks of the CSLA block mask: row g (shared by every (b, h)) of

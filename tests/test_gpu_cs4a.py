@@ -76,6 +76,15 @@ def test_infinity_schedule_blocks_of_128():
     cs4a_case(INF_SIDES, 8, 4, 10, [11, 12, 13], 1, 2, 128, 32, 128, 256, 41)
 
 
+@pytest.mark.parametrize("chunk", ["32", "64"])
+@pytest.mark.parametrize("C", [64, 128])
+def test_gather_chunks_of_32_and_64_keys(monkeypatch, chunk, C):
+    # both chunk shapes of the gather attention at d = 128 (two and four waves),
+    # for the O_cache pass at S and the later steps
+    monkeypatch.setenv("SPARVAR_CS4A_CHUNK", chunk)
+    cs4a_case(INF_SIDES, 8, 4, 10, [11, 13], 1, 2, 128, 32, C, 200, 46 + C, heads=[1])
+
+
 def test_blocks_of_64_without_cache_and_d64():
     h = [1, 2, 3, 5, 7, 10, 13, 20]
     cs4a_case(h, 4, 2, 6, [7, 8], 2, 2, 64, 8, 64, 40, 42, with_cache=False)
