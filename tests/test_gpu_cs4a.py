@@ -76,6 +76,13 @@ def test_infinity_schedule_blocks_of_128():
     cs4a_case(INF_SIDES, 8, 4, 10, [11, 12, 13], 1, 2, 128, 32, 128, 256, 41)
 
 
+def test_infinity_layer_full_size_sampled_heads():
+    # the swept token-path workload: B = 2, H = 16, d = 128, query blocks of 128,
+    # top-1024 tokens, steps 40/48/64 (automatic chunk shapes); every index list
+    # and top-K bit-exact, attention checked on two heads
+    cs4a_case(INF_SIDES, 8, 4, 10, [11, 12, 13], 2, 16, 128, 32, 128, 1024, 49, heads=[0, 31])
+
+
 @pytest.mark.parametrize("chunk", ["32", "64"])
 @pytest.mark.parametrize("C", [64, 128])
 def test_gather_chunks_of_32_and_64_keys(monkeypatch, chunk, C):
