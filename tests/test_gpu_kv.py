@@ -72,3 +72,28 @@ def test_csla_on_the_compressed_cache():
         vcmp = O.kv_compact(v[0, bh], og, keep)
         ref, _ = O.csla_attention(q[0, bh, og.C(k - 1):og.C(k)], kcmp, vcmp, want_rows, block, scale_of(d))
         assert_close(o.float().cpu().numpy()[0, bh], ref, "bf16", f"compressed cache head {bh}")
+
+
+def test_compact_full_size_24_heads():
+    # the measured workload: batch 1, 24 heads, d = 128, the 10521-token cache of
+    # the Infinity schedule compressed to its sink and windowed scales (8121 tokens)
+    h, d, H = INF_SIDES, 128, 24
+    keep = [1, 2, 3, 4, 5, 11, 12, 13]
+    og = O.Geometry(h, h, 8, 5)
+    g = sv.Geometry(h, h, 8, 5)
+    note(f"[kv] compact full size H={H} keep={keep}")
+    r = np.random.default_rng(63)
+    n = og.C(13)
+    Ks = torch.from_numpy(r.standard_normal((1, H, n, d)).astype(np.float32)).to(torch.bfloat16).cuda()
+    Vs = torch.from_numpy(r.standard_normal((1, H, n, d)).astype(np.float32)).to(torch.bfloat16).cuda()
+    m = sum(og.N(l) for l in keep)
+    assert m == 8121
+    Kd = torch.empty(1, H, m, d, dtype=torch.bfloat16, device="cuda")
+    Vd = torch.empty_like(Kd)
+    sv.sparvar_kv_compact(g, keep, Ks, Vs, Kd, Vd)
+    torch.cuda.synchronize()
+    ks, vs = Ks.view(torch.int16).cpu().numpy(), Vs.view(torch.int16).cpu().numpy()
+    kd, vd = Kd.view(torch.int16).cpu().numpy(), Vd.view(torch.int16).cpu().numpy()
+    for hh in range(H):
+        assert np.array_equal(kd[0, hh], O.kv_compact(ks[0, hh], og, keep))
+        assert np.array_equal(vd[0, hh], O.kv_compact(vs[0, hh], og, keep))
