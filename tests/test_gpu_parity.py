@@ -259,3 +259,31 @@ def test_deterministic_and_schedule_invariant():
     path.attn_step(13, Q, K, V, use_schedule=False)
     torch.cuda.synchronize()
     assert torch.equal(first, path.out[13])
+
+
+@pytest.mark.parametrize("group_waves", ["0", "4"])
+def test_full_rows_past_the_chunk_table(monkeypatch, group_waves):
+    # every 8x8 tile of the 64x64 scale lists all 172 blocks of the Infinity cache:
+    # 344 chunks of 32 keys per row, past the 256-entry chunk table (refills), and
+    # for pairs of tiles past the row-merge capacity (served tile by tile); the
+    # result is dense attention over the 10521-token cache
+    monkeypatch.setenv("SPARVAR_SPARSE_GROUP_WAVES", group_waves)
+    h, d = INF_SIDES, 128
+    note(f"[parity] full rows at 64x64, group waves {group_waves}")
+    g = sv.Geometry(h, h, 8, 4)
+    og = oracle_geometry(h, h, 8, 4)
+    q, k, v = make_case(h, h, 1, 2, d, 32, 4, 64, "bf16")
+    NB, G = og.nb_le(13), og.tiles(13)
+    rows = 2 * G
+    rp = torch.arange(0, (rows + 1) * NB, NB, dtype=torch.int32, device="cuda")
+    ci = torch.arange(NB, dtype=torch.int32, device="cuda").repeat(rows)
+    n0, n1 = og.C(12), og.C(13)
+    Q = to_dev(q[:, :, n0:n1], "bf16")
+    K, V = to_dev(k, "bf16"), to_dev(v, "bf16")
+    o = torch.empty_like(Q)
+    sv.sparvar_block_sparse_attn_fwd(g, 13, Q, K, V, o, rp, ci, softmax_scale=scale_of(d))
+    torch.cuda.synchronize()
+    got = o.float().cpu().numpy()
+    for bh in range(2):
+        ref, _ = O.dense_attention(q[0, bh, n0:n1], k[0, bh], v[0, bh], scale_of(d))
+        assert_close(got[0, bh], ref, "bf16", f"full rows head {bh}")
