@@ -38,7 +38,8 @@
  *  - Supported: d in {64, 128}; dtype bf16 (bf16 MFMA, fp32 softmax and
  *    accumulation, bf16 output rounded to nearest even) or fp32 (fp32 MFMA).
  *  - Limits: 1 <= num_scales <= SPARVAR_MAX_SCALES, 1 <= block_edge <= 64,
- *    total cache tokens < 2^31, B * H * rows < 2^31.
+ *    scale sides <= SPARVAR_MAX_SIDE, total cache tokens < 2^31,
+ *    B * H * rows < 2^31.
  *
  * Return value: SPARVAR_OK (0) or a negative status; a message for the last
  * failure on the calling thread is available from sparvar_last_error().
@@ -64,6 +65,7 @@ extern "C" {
 #endif
 
 #define SPARVAR_MAX_SCALES 32
+#define SPARVAR_MAX_SIDE 65535
 
 enum sparvar_status {
   SPARVAR_OK = 0,

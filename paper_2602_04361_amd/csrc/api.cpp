@@ -72,6 +72,9 @@ int build_table(const sparvar_geometry_t* g, GeoTable* T) {
   for (int i = 0; i < T->L; ++i) {
     const int32_t h = g->h[i], w = g->w[i];
     if (h < 1 || w < 1) return fail(SPARVAR_ERR_INVALID, "scale %d has size %dx%d", i + 1, h, w);
+    // chunk descriptors keep a tile's row pitch (the scale width) in 16 bits
+    if (h > SPARVAR_MAX_SIDE || w > SPARVAR_MAX_SIDE)
+      return fail(SPARVAR_ERR_INVALID, "scale %d has a side over %d (%dx%d)", i + 1, SPARVAR_MAX_SIDE, h, w);
     T->h[i] = h;
     T->w[i] = w;
     T->eh[i] = h < T->b ? h : T->b;

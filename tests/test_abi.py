@@ -89,6 +89,11 @@ def test_geometry_validation():
     for h, b in [([0, 2], 8), ([1, 2], 0), ([1, 2], 65), (list(range(1, 40)), 8)]:
         g = sv.Geometry(h, h, b, 1)
         assert lib.sparvar_scale_info(g.ref, 1, ctypes.byref(info)) == sv.ERR_INVALID
+    # a side over 65535 (the chunk descriptors keep a row pitch in 16 bits)
+    g = sv.Geometry([1, 1], [1, 65536], 8, 1)
+    assert lib.sparvar_scale_info(g.ref, 1, ctypes.byref(info)) == sv.ERR_INVALID
+    g = sv.Geometry([1, 1], [1, 65535], 8, 1)
+    assert lib.sparvar_scale_info(g.ref, 2, ctypes.byref(info)) == sv.OK
     g = sv.Geometry([1, 2], [1, 2], 8, 1)
     assert lib.sparvar_scale_info(g.ref, 3, ctypes.byref(info)) == sv.ERR_INVALID
 
