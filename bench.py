@@ -482,7 +482,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the path shards by (batch, head) "
-              f"with no exchange inside attention, but this build measures a single GPU.", file=sys.stderr)
+              f"with no exchange inside attention, and the benchmark measures one GPU's share.", file=sys.stderr)
         sys.exit(2)
     import torch
 
