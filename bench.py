@@ -169,8 +169,8 @@ def traffic_from_profile(kernel_hash):
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for name in ("attention.hip", "device_common.h", "geometry.h"):
-        with open(os.path.join(ROOT, "paper_2602_04361_amd", "csrc", name), "rb") as f:
+    for name in ("csrc/attention.hip", "csrc/device_common.h", "csrc/geometry.h", "build.py"):  # build.py: the flags
+        with open(os.path.join(ROOT, "paper_2602_04361_amd", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
 

@@ -35,17 +35,25 @@ struct Chunk {
   uint32_t mask;
 };
 
-// Both products use the 24-bit multiplier, which issues at full rate where a
-// 32-bit integer multiply issues at quarter rate; every factor fits in 24 bits
-// (s < 64, magic <= 65536, 0 <= stride - nc < 65536).
+// Both products must use the 24-bit multiplier, which issues at full rate where
+// a 32-bit integer multiply issues at quarter rate. Every factor fits (s < 64,
+// magic <= 65536, 0 <= stride - nc < 65536); the row advance is masked to 16
+// bits so that the compiler can see it too.
 __device__ __forceinline__ int32_t chunk_token(const Chunk& c, int32_t s) {
   const uint32_t q = __umul24((uint32_t)s, (uint32_t)c.magic) >> 16;
-  return c.base + s + (int32_t)__umul24(q, (uint32_t)(c.stride - c.nc));
+  const uint32_t adv = (uint32_t)(c.stride - c.nc) & 0xffffu;
+  return c.base + s + (int32_t)(q * adv);
 }
 
-// Slot a copying lane reads: slots past the chunk's count read its first key
-// (their scores are masked), so every lane issues the same copies.
-__device__ __forceinline__ int32_t chunk_slot(int32_t s, int32_t count) { return s < count ? s : 0; }
+// Slot a copying lane reads: slots past the chunk's count read its last key
+// (their scores are masked), so every lane issues the same copies. One unsigned
+// minimum against a wave-uniform bound below 64 (count <= 64), which also tells
+// the compiler that the slot fits the 24-bit multiplier.
+__device__ __forceinline__ int32_t chunk_slot(int32_t s, int32_t count) {
+  const uint32_t last = (uint32_t)(count > 1 ? count - 1 : 0) & 63u;
+  const uint32_t u = (uint32_t)s;
+  return (int32_t)(u < last ? u : last);
+}
 
 // ceil(65536 / n) for n = 0..64 (entry 0 unused).
 __constant__ const uint32_t kNcMagic[65] = {
