@@ -169,6 +169,22 @@ def test_schedule_2048_sampled():
              tiles_per_step=12)
 
 
+def test_infinity_wide_32_heads_full_size():
+    # the wider variant: B=2, H=32 (64 planes), same schedule and sparsity rules.
+    # Every index list bit-exact on all heads; attention sampled on three heads.
+    run_case(INF_SIDES, INF_SIDES, 8, 4, 10, [11, 12, 13], 2, 32, 128, 32, 8, 1, "bf16", seed=2,
+             heads=[0, 45, 63], tiles_per_step=8)
+
+
+@pytest.mark.parametrize("b,topk,r", [(8, 4, 2), (8, 32, 1), (16, 4, 1), (16, 32, 2)])
+def test_sparsity_sweep_settings_full_size(b, topk, r):
+    # the sparsity sweep's settings on the Infinity layer (B=2, H=16, d=128): top-k
+    # 4 and 32, blocks of 8x8 and 16x16 tokens, local radius 1 and 2. Index lists
+    # bit-exact on all heads; attention sampled on two heads.
+    run_case(INF_SIDES, INF_SIDES, b, 4, 10, [11, 12, 13], 2, 16, 128, 32, topk, r, "bf16", seed=40 + topk + r,
+             heads=[3, 26], tiles_per_step=6)
+
+
 # ---------------------------------------------------------------- dense kernel edge cases
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("n_q,n_kv,d", [(1, 1, 64), (33, 65, 64), (100, 333, 128), (257, 129, 128)])
