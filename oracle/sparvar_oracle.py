@@ -43,6 +43,7 @@ __all__ = [
     "topk_blocks",
     "homography",
     "map_block",
+    "map_block_cover",
     "sink_blocks",
     "local_blocks",
     "build_rows",
@@ -291,6 +292,40 @@ def map_block(geom, v, S, k):
     return geom.block_id(lp, up // geom.eh(lp), wp // geom.ew(lp))
 
 
+def _upsampled_tiles(geom, l, lp, t, axis):
+    """Scale-lp tile range along one axis covered by the upsampled span of tile t of scale l."""
+    if axis == 0:
+        e, n, e_p, n_p = geom.eh(l), geom.hh(l), geom.eh(lp), geom.hh(lp)
+    else:
+        e, n, e_p, n_p = geom.ew(l), geom.ww(l), geom.ew(lp), geom.ww(lp)
+    x0, x1 = t * e, min((t + 1) * e, n)         # the tile's tokens along the axis, [x0, x1)
+    lo = (x0 * n_p) // n                        # first target token of the span x0 n_p / n ...
+    hi = -(-(x1 * n_p) // n)                    # ... and the end of x1 n_p / n, rounded up (exclusive)
+    return lo // e_p, (hi - 1) // e_p
+
+
+def map_block_cover(geom, v, S, k):
+    """Decompose-Align-Project of one selected block, covering form.
+
+    Decompose and Align as in map_block (scale l -> l' = k - (S - l)). Project
+    follows the Spatial Projection step token by token, u -> floor(u h_l'/h_l):
+    the tile's tokens [x0, x1) x [y0, y1) of scale l occupy the upsampled span
+    [x0 h_l'/h_l, x1 h_l'/h_l) x [y0 w_l'/w_l, y1 w_l'/w_l) of scale l', and the
+    mapped blocks are every scale-l' tile overlapping that span. A selected
+    region thus keeps its share of its scale's area on the larger scale (the
+    kept keys stay about alpha of the cache, as the complexity appendix
+    assumes), where the point form keeps the count of blocks. The point form's
+    tile is always among them. Returns the ascending block ids.
+    """
+    l, tu, tv = geom.decompose_block(v)
+    if l > S:
+        raise ValueError("block is not in the cache at step S")
+    lp = k - (S - l)
+    r0, r1 = _upsampled_tiles(geom, l, lp, tu, 0)
+    c0, c1 = _upsampled_tiles(geom, l, lp, tv, 1)
+    return [geom.block_id(lp, a, c) for a in range(r0, r1 + 1) for c in range(c0, c1 + 1)]
+
+
 def sink_blocks(geom):
     """Every block of the first n_sink scales (the Attention Sink paragraph:
     the first N_sink tokens stay visible to all queries)."""
@@ -340,15 +375,18 @@ def local_blocks(geom, k, radius, prev_dilation=0):
     return rows
 
 
-def build_rows(geom, S, k, topk_idx, local_rows):
+def build_rows(geom, S, k, topk_idx, local_rows, projection="point"):
     """Kept-block lists at step k for every (batch*head, query tile).
 
     inds^(k) = A_sink U M_{S->k}(inds^(S)) (Attention Sink paragraph), united
     with the local window. The source tile of target tile (a, c) is
     (homography(a), homography(c)); each of its selected blocks goes through
-    map_block. ``topk_idx`` is int [BH, G_S, topk] with -1 padding.
+    map_block (projection "point") or map_block_cover ("cover").
+    ``topk_idx`` is int [BH, G_S, topk] with -1 padding.
     Returns rows[bh][g] as ascending unique lists.
     """
+    if projection not in ("point", "cover"):
+        raise ValueError("projection is 'point' or 'cover'")
     topk_idx = np.asarray(topk_idx)
     BH = topk_idx.shape[0]
     out = []
@@ -361,7 +399,10 @@ def build_rows(geom, S, k, topk_idx, local_rows):
                 s = set(local_rows[g])
                 for vb in topk_idx[bh, gs]:
                     if vb >= 0:
-                        s.add(map_block(geom, int(vb), S, k))
+                        if projection == "point":
+                            s.add(map_block(geom, int(vb), S, k))
+                        else:
+                            s.update(map_block_cover(geom, int(vb), S, k))
                 per.append(sorted(s))
         out.append(per)
     return out

@@ -24,6 +24,7 @@ from oracle import (
     local_blocks,
     longest_first,
     map_block,
+    map_block_cover,
     masked_attention,
     pooled_scores,
     rows_to_csr,
@@ -458,3 +459,108 @@ def test_footprint_is_positive_measure_overlap():
                     want = [t for t in range(g.Th(1)) if t * e_p < hi and min((t + 1) * e_p, n_p) > lo]
                     got = sorted(g.decompose_block(v)[1] for v in rows[a] if g.decompose_block(v)[0] == 1)
                     assert got == want, (n_k, n_p, b, a)
+
+
+# ---------------------------------------------------------------- covering projection
+def test_cover_projection_hand_tables(golden_dir):
+    for case in load(golden_dir, "hand_tables.json")["projection_cover"]["cases"]:
+        # scale l = 2 of a square 3-scale schedule at step S=2, mapped to step k=3 (l' = 3), b = 8
+        g = Geometry([1, case["h_l"], case["h_lp"]], [1, case["h_l"], case["h_lp"]], 8, 0)
+        c_lo, c_hi = case["tile_ranges"][0]  # column span of the source column tile 0
+        for tu, (lo, hi) in zip(case["tiles"], case["tile_ranges"]):
+            want = [g.block_id(3, a, c) for a in range(lo, hi + 1) for c in range(c_lo, c_hi + 1)]
+            assert map_block_cover(g, g.block_id(2, tu, 0), 2, 3) == want, (case, tu)
+
+
+def _cover_geometries():
+    inf = [1, 2, 4, 6, 8, 12, 16, 20, 24, 32, 40, 48, 64]
+    return [Geometry(inf, inf, 8, 4), Geometry(inf, inf, 16, 4), Geometry(inf + [80, 96, 128], inf + [80, 96, 128], 8, 4),
+            Geometry([1, 2, 3, 5, 7, 10, 13], [1, 3, 4, 7, 9, 14, 21], 3, 1),
+            Geometry([1, 2, 3, 5, 7, 10, 13], [1, 3, 4, 7, 9, 14, 21], 2, 0)]
+
+
+def test_cover_contains_point_map_identity_and_monotone():
+    for g in _cover_geometries():
+        for S in range(1, g.L + 1):
+            for v in range(g.nb_le(S)):
+                assert map_block_cover(g, v, S, S) == [v]  # no scale change: the tile itself
+            for k in range(S + 1, g.L + 1):
+                for v in range(g.nb_le(S)):
+                    cov = map_block_cover(g, v, S, k)
+                    assert cov == sorted(set(cov)) and map_block(g, v, S, k) in cov
+                    l, tu, tv = g.decompose_block(v)
+                    assert all(g.decompose_block(x)[0] == k - (S - l) for x in cov)
+                # tile ranges move forward with the source tile, per axis
+                for l in range(1, S + 1):
+                    lp = k - (S - l)
+                    firsts = [g.decompose_block(map_block_cover(g, g.block_id(l, tu, 0), S, k)[0])[1]
+                              for tu in range(g.Th(l))]
+                    lasts = [g.decompose_block(map_block_cover(g, g.block_id(l, tu, 0), S, k)[-1])[1]
+                             for tu in range(g.Th(l))]
+                    assert firsts == sorted(firsts) and lasts == sorted(lasts) and lasts[-1] == g.Th(lp) - 1
+
+
+def test_cover_is_positive_area_overlap_of_the_upsampled_tile():
+    # brute force in exact rationals: a scale-l' tile is covered iff its extent meets
+    # the upsampled span of the source tile with positive area
+    for h, w, b in [([1, 2, 3, 5, 7, 10, 13], [1, 3, 4, 7, 9, 14, 21], 3), ([1, 2, 4, 6, 9, 12], [1, 2, 4, 6, 9, 12], 4),
+                    ([1, 3, 5, 8, 11], [2, 3, 7, 10, 16], 2)]:
+        g = Geometry(h, w, b, 1)
+        for S in range(1, g.L):
+            for k in range(S + 1, g.L + 1):
+                for v in range(g.nb_le(S)):
+                    l, tu, tv = g.decompose_block(v)
+                    lp = k - (S - l)
+                    rh, rw = Fraction(g.hh(lp), g.hh(l)), Fraction(g.ww(lp), g.ww(l))
+                    x0, x1 = tu * g.eh(l), min((tu + 1) * g.eh(l), g.hh(l))
+                    y0, y1 = tv * g.ew(l), min((tv + 1) * g.ew(l), g.ww(l))
+                    want = []
+                    for a in range(g.Th(lp)):
+                        for c in range(g.Tw(lp)):
+                            a0, a1 = a * g.eh(lp), min((a + 1) * g.eh(lp), g.hh(lp))
+                            c0, c1 = c * g.ew(lp), min((c + 1) * g.ew(lp), g.ww(lp))
+                            if max(a0, x0 * rh) < min(a1, x1 * rh) and max(c0, y0 * rw) < min(c1, y1 * rw):
+                                want.append(g.block_id(lp, a, c))
+                    assert map_block_cover(g, v, S, k) == want, (h, w, b, S, k, v)
+
+
+def test_cover_keeps_the_selected_share_of_each_scale():
+    # the blocks of a scale cover the aligned scale exactly, and any selection keeps at
+    # least its share of its scale's tokens on the larger scale (kept keys stay about
+    # alpha of the cache), while the point form keeps only the count of blocks
+    rng = np.random.default_rng(3)
+    for g in _cover_geometries():
+        for S in range(2, g.L):
+            for k in range(S + 1, g.L + 1):
+                for l in range(1, S + 1):
+                    lp = k - (S - l)
+                    blocks = [g.block_id(l, a, c) for a in range(g.Th(l)) for c in range(g.Tw(l))]
+                    every = set()
+                    for v in blocks:
+                        every.update(map_block_cover(g, v, S, k))
+                    assert every == set(range(g.base(lp), g.base(lp) + g.tiles(lp)))
+                    for _ in range(3):
+                        sel = [v for v in blocks if rng.random() < 0.3] or blocks[:1]
+                        cov = set()
+                        for v in sel:
+                            cov.update(map_block_cover(g, v, S, k))
+                        share_src = Fraction(sum(len(g.block_tokens(v)) for v in sel), g.N(l))
+                        share_dst = Fraction(sum(len(g.block_tokens(v)) for v in cov), g.N(lp))
+                        assert share_dst >= share_src
+
+
+def test_build_rows_cover_is_a_superset_of_point():
+    inf = [1, 2, 4, 6, 8, 12, 16, 20, 24, 32, 40, 48, 64]
+    g = Geometry(inf, inf, 8, 4)
+    rng = np.random.default_rng(11)
+    topk = np.sort(np.stack([rng.choice(g.nb_le(10), 8, replace=False) for _ in range(2 * g.tiles(10))]), axis=1)
+    topk = topk.reshape(2, g.tiles(10), 8)
+    for k in (11, 12, 13):
+        loc = local_blocks(g, k, 1)
+        point = build_rows(g, 10, k, topk, loc)
+        cover = build_rows(g, 10, k, topk, loc, projection="cover")
+        for bh in range(2):
+            for t in range(g.tiles(k)):
+                assert set(point[bh][t]) <= set(cover[bh][t]) and cover[bh][t] == sorted(set(cover[bh][t]))
+        with pytest.raises(ValueError):
+            build_rows(g, 10, k, topk, loc, projection="area")
