@@ -12,9 +12,11 @@ One step = one layer of the whole hot path on the Infinity 1024x1024 schedule
 Inputs are seeded synthetic tensors resident in HBM; four input sets rotate so
 no step finds its K/V in cache from the previous one.
 
-Prints one JSON line. `value` is the algorithmic TFLOP/s of the whole step
-(4 d * attended query-key pairs: the dense decision scale plus the kept pairs
-of the three sparse steps) over the measured step time.
+Prints one JSON line. `value` is the algorithmic TFLOP/s of the block-sparse
+attention at the 64x64 step (4 d * kept query-key pairs over its measured
+duration inside the step), the metric's subject; `ms_per_layer` is the whole
+step and `layer_tflops` its algorithmic rate (the dense decision scale plus the
+kept pairs of the three sparse steps).
 """
 from __future__ import annotations
 
@@ -114,6 +116,7 @@ def cpu_baseline(q, k, v, target_s):
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         threads = 1
+    affinity = len(os.sched_getaffinity(0))
     B, H, d = CFG["B"], CFG["H"], CFG["d"]
     g = O.Geometry(SIDES, SIDES, CFG["b"], CFG["n_sink"])
     S = CFG["S"]
@@ -143,28 +146,42 @@ def cpu_baseline(q, k, v, target_s):
             break
     dt = time.perf_counter() - t0
     return {"value": flops_done / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "blas_threads": int(threads), "affinity_cores": affinity,
             "sample": f"whole step (decision + 3 sparse steps) for {heads} of {BH} (batch, head) planes, "
-                      f"fp64 NumPy, {dt:.1f} s"}
+                      f"fp64 NumPy, {dt:.1f} s; {threads} BLAS threads on {affinity} cores in the affinity mask"}
 
 
-def traffic_from_profile(kernel_hash):
-    """HBM bytes per launch of the sparse kernel from the committed rocprofv3 PMC
-    summary, if it was taken on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", "sparse_attn_64_traffic.txt")
+def profile_value(name, key, kernel_hash):
+    """A per-launch figure of the 64x64 sparse kernel from a committed rocprofv3
+    PMC summary under profiles/, if it was taken on the current kernel source;
+    else None."""
+    path = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(path):
         return None
     vals = {}
     with open(path) as f:
         for line in f:
             if "=" in line and not line.startswith("#"):
-                key, val = line.split("=", 1)
-                vals[key.strip()] = val.strip()
+                k_, val = line.split("=", 1)
+                vals[k_.strip()] = val.strip()
     if vals.get("kernel_source_sha256") != kernel_hash:
         return None
     try:
-        return float(vals["hbm_bytes_per_launch"])
+        return float(vals[key])
     except (KeyError, ValueError):
         return None
+
+
+def own_block_rows(info, k, BH):
+    """CSR in which every query tile of scale k lists only its own block: each
+    K/V token of scale k is read by exactly one workgroup (no re-reads), so the
+    launch's compulsory HBM bytes are known exactly (Q + K/V of scale k + O)."""
+    G = info[k]["tiles_h"] * info[k]["tiles_w"]
+    base = info[k]["block_offset"]
+    rows = BH * G
+    row_ptr = np.arange(rows + 1, dtype=np.int32)
+    col_idx = (base + np.tile(np.arange(G, dtype=np.int32), BH)).astype(np.int32)
+    return row_ptr, col_idx
 
 
 def kernel_source_hash():
@@ -592,6 +609,20 @@ def main():
     dense64_ms = e0.elapsed_time(e1) / dn
     dense64_flops = 4.0 * d * BH * i13["n_tokens"] * i13["n_tokens_le"]
 
+    # warm number, labelled as such: the 64x64 sparse attention repeated on one
+    # input set (its K/V partly cache-resident from the previous launch)
+    Q0, K0, V0 = sets[0]
+    one_step(0)  # the rows of set 0, which the accounting used
+    torch.cuda.synchronize()
+    wn = 20
+    we = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(wn)]
+    for a_, b_ in we:
+        a_.record(stream)
+        path.attn_step(13, Q0, K0, V0, use_order=True)
+        b_.record(stream)
+    torch.cuda.synchronize()
+    warm13_ms = float(np.median([a_.elapsed_time(b_) for a_, b_ in we]))
+
     f13, b13, dens13, _ = acct[13]
     attn13_ms = per["attn_13"]
     kernels = {"decision": {"ms": per["decision"], "tflops": dense_S_flops / per["decision"] / 1e9,
@@ -607,11 +638,19 @@ def main():
                                    "hbm_gbs_algorithmic": b_ / per[f"attn_{kk}"] / 1e6,
                                    "density": dens, "kept_keys_per_row_mean": float(np.mean(keys))}
     dominant = max(kernels, key=lambda n: kernels[n]["ms"])
-    traffic = traffic_from_profile(kernel_source_hash())
+    khash = kernel_source_hash()
+    traffic = profile_value("sparse_attn_64_traffic.txt", "hbm_bytes_per_launch", khash)
+    issued = profile_value("sparse_attn_64_mfma.txt", "mfma_flops_per_launch", khash)
     achieved = f13 / attn13_ms / 1e9
-    roofline = {"kernel": "block-sparse attention, 64x64 step", "bound": "mfma", "achieved": achieved,
-                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
+    # the roof that bounds the kernel at its algorithmic intensity: MFMA above the
+    # ridge (peak FLOP/s over peak bytes/s), HBM below it
+    intensity = f13 / b13
+    ridge = PEAK_BF16_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    roofline = {"kernel": "block-sparse attention, 64x64 step", "bound": "mfma" if intensity >= ridge else "hbm",
+                "achieved": achieved, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                 "traffic": traffic, "algorithmic_bytes": b13, "algorithmic_flops": f13,
+                "intensity_flop_per_byte": intensity, "ridge_flop_per_byte": ridge,
+                "hbm_frac_algorithmic": b13 / attn13_ms / 1e6 / PEAK_HBM_GBS,
                 "dominant_kernel_in_step": dominant}
 
     if args.copy_calibration:
@@ -624,6 +663,22 @@ def main():
         torch.cuda.synchronize()
         print(f"[bench] copy calibration: 3 x {src.numel() * 4} bytes read and written", file=sys.stderr, flush=True)
         del src, dst
+        # the same check on the attention kernel itself: every tile of the 64x64 step
+        # lists only its own block, so each K/V token is read once (last dispatches of
+        # the sparse kernel in the run)
+        rp_np, ci_np = own_block_rows(info, 13, BH)
+        rp_c = torch.from_numpy(rp_np).to(dev)
+        ci_c = torch.from_numpy(ci_np).to(dev)
+        o_c = torch.empty(B, H, i13["n_tokens"], d, dtype=torch.bfloat16, device=dev)
+        for i in range(2):
+            Q, K, V = sets[(i + 1) % len(sets)]
+            sv.sparvar_block_sparse_attn_fwd(g, 13, path.q_slice(Q, 13), path.kv_prefix(K, 13),
+                                             path.kv_prefix(V, 13), o_c, rp_c, ci_c, softmax_scale=path.scale)
+        torch.cuda.synchronize()
+        cb = BH * i13["n_tokens"] * d * 2
+        print(f"[bench] attention calibration: 2 launches, each reading {3 * cb} bytes (Q + K + V of scale 13) and "
+              f"writing {cb} bytes (O)", file=sys.stderr, flush=True)
+        del o_c
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -631,7 +686,7 @@ def main():
 
     line = {
         "metric": "ms/layer + effective TFLOP/s (% bf16 MFMA peak) sparse attn at 64x64 scale",
-        "value": step_flops / ms_step / 1e9,
+        "value": achieved,
         "unit": "TFLOP/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -646,12 +701,20 @@ def main():
                                "block-sparse steps 40x40/48x48/64x64", "batch": B, "heads": H, "head_dim": d,
                    "block": "8x8 tokens", "topk": CFG["topk"], "window_radius": CFG["radius"],
                    "sink_scales": CFG["n_sink"], "kv_tokens_last_step": info[13]["n_tokens_le"]},
+        "value_is": "algorithmic TFLOP/s of the block-sparse attention at the 64x64 step, timed inside the step",
         "ms_per_layer": ms_step,
+        "layer_tflops": step_flops / ms_step / 1e9,
         "ms_per_step_spread": {"median": float(np.median(step_ms)), "p10": float(np.percentile(step_ms, 10)),
                                "p90": float(np.percentile(step_ms, 90))},
         "sparse_64": {"ms": attn13_ms, "tflops": achieved, "frac_bf16_peak": achieved / PEAK_BF16_TFLOPS,
+                      "dense_equivalent_tflops": dense64_flops / attn13_ms / 1e9,
+                      "mfma_issued_flops": issued,
+                      "mfma_padding_efficiency": (f13 / issued) if issued else None,
+                      "warm_same_buffers_ms": warm13_ms,
+                      "warm_same_buffers_tflops": f13 / warm13_ms / 1e9,
                       "density": dens13, "dense_ms": dense64_ms,
                       "dense_tflops": dense64_flops / dense64_ms / 1e9,
+                      "dense_frac_bf16_peak": dense64_flops / dense64_ms / 1e9 / PEAK_BF16_TFLOPS,
                       "speedup_vs_own_dense": dense64_ms / attn13_ms},
         "kernels": kernels,
         "roofline": roofline,

@@ -27,32 +27,35 @@
  *    scale-major and row-major over tiles inside a scale. Query tiles of
  *    scale k use the same tiling ("query blocks" of the paper).
  *  - Every pointer except the geometry is device memory owned by the caller.
- *    The library allocates no device memory, keeps no global state and never
- *    synchronises: work is enqueued on `stream` (NULL = the default stream)
- *    and results are valid once the caller has synchronised that stream.
+ *    The library allocates no device memory and never synchronises: work is
+ *    enqueued on `stream` (NULL = the default stream) and results are valid
+ *    once the caller has synchronised that stream.
+ *  - Process-wide state: the message of the last failure (one per calling
+ *    thread), the compute-unit count of each device (queried once, used by the
+ *    automatic launch shapes) and the launch options of
+ *    sparvar_set_launch_option. Calls are safe from several threads and
+ *    streams; a launch option changed while another thread launches takes
+ *    effect for that call or the next.
  *  - Every call validates its arguments on the host before enqueueing any
  *    work; on error nothing is written. Device data (index lists, block ids)
  *    is not read on the host; kernels skip block ids that are out of range.
- *  - Inputs must be finite. Outputs are bitwise deterministic for fixed
- *    inputs and launch arguments.
+ *  - Inputs must be finite and softmax_scale finite and > 0 (the bf16 kernels
+ *    take the running maximum of the raw scores and scale it afterwards).
+ *    Outputs are bitwise deterministic for fixed inputs, launch arguments
+ *    and launch options.
  *  - Supported: d in {64, 128}; dtype bf16 (bf16 MFMA, fp32 softmax and
  *    accumulation, bf16 output rounded to nearest even) or fp32 (fp32 MFMA).
  *  - Limits: 1 <= num_scales <= SPARVAR_MAX_SCALES, 1 <= block_edge <= 64,
  *    scale sides <= SPARVAR_MAX_SIDE, total cache tokens < 2^31,
- *    B * H * rows < 2^31.
+ *    B * H * rows < 2^31; for bf16, one (b, h) plane of K or V (cache tokens
+ *    x d x 2 bytes) below 2^32 bytes, i.e. fewer than 2^24 cache tokens at
+ *    d = 128 (the HBM -> LDS copies use 32-bit offsets into a plane).
  *
  * Return value: SPARVAR_OK (0) or a negative status; a message for the last
  * failure on the calling thread is available from sparvar_last_error().
  *
- * Launch shapes are chosen automatically. For measurements, environment
- * variables read at each call override them: SPARVAR_DENSE_WAVES / _CHUNK /
- * _STAGES (dense attention), SPARVAR_SPARSE_WAVES / _CHUNK / _STAGES and
- * SPARVAR_SPARSE_GROUP_WAVES / _GROUP_CHUNK / _GROUP_STAGES (block-sparse
- * attention; group waves 0 = one query tile per workgroup), SPARVAR_CSLA_CHUNK
- * / _STAGES, SPARVAR_CS4A_CHUNK (token gather attention), SPARVAR_DECISION_FUSED
- * and SPARVAR_SWIZZLE (0 = natural workgroup order). A shape that is not built
- * falls back to the default; results do not depend on the shape beyond
- * floating-point summation order.
+ * Launch shapes are chosen automatically; sparvar_set_launch_option overrides
+ * them process-wide (for measurements and tests).
  */
 #ifndef SPARVAR_H_
 #define SPARVAR_H_
@@ -76,6 +79,33 @@ enum sparvar_status {
 };
 
 typedef enum sparvar_dtype { SPARVAR_BF16 = 0, SPARVAR_F32 = 1 } sparvar_dtype_t;
+
+/* Launch options: process-wide overrides of the automatic launch shapes. A
+ * shape that is not built falls back to the default; results depend on the
+ * options only through floating-point summation order (index lists never). */
+typedef enum sparvar_launch_option {
+  SPARVAR_OPT_SWIZZLE = 0,         /* 1 (default): XCD-aware workgroup order; 0: natural order */
+  SPARVAR_OPT_DENSE_WAVES,         /* dense attention: waves per workgroup, 0 (default) = automatic */
+  SPARVAR_OPT_DENSE_CHUNK,         /* keys per staged chunk, 64 (default) or 32 */
+  SPARVAR_OPT_DENSE_STAGES,        /* LDS pipeline stages, 2 (default) to 4 */
+  SPARVAR_OPT_SPARSE_WAVES,        /* block-sparse attention: waves, 0 (default) = from the tile size */
+  SPARVAR_OPT_SPARSE_CHUNK,        /* 32 (default) or 64 */
+  SPARVAR_OPT_SPARSE_STAGES,       /* 2 (default) to 4 */
+  SPARVAR_OPT_SPARSE_GROUP_WAVES,  /* -1 (default) = automatic, 0 = one query tile per workgroup, 4 or 8 */
+  SPARVAR_OPT_SPARSE_GROUP_CHUNK,  /* 64 (default) or 32 */
+  SPARVAR_OPT_SPARSE_GROUP_STAGES, /* 2 (default) to 4 */
+  SPARVAR_OPT_CSLA_CHUNK,          /* CSLA block path: 32 (default) or 64 */
+  SPARVAR_OPT_CSLA_STAGES,         /* 2 (default) to 4 */
+  SPARVAR_OPT_CS4A_CHUNK,          /* token gather attention: -1 (default) = automatic, 32 or 64 */
+  SPARVAR_OPT_DECISION_FUSED,      /* sparvar_decision_step: -1 (default) = automatic, 1 = fused whenever
+                                      supported, 0 = two-call sequence */
+  SPARVAR_OPT_COUNT
+} sparvar_launch_option_t;
+#define SPARVAR_OPT_DEFAULT INT32_MIN /* value that restores an option's default */
+
+/* Set (or, with SPARVAR_OPT_DEFAULT, reset) one launch option; read one. */
+int sparvar_set_launch_option(int32_t option, int32_t value);
+int sparvar_get_launch_option(int32_t option, int32_t* value);
 
 /* Scale schedule and tiling. h[l-1], w[l-1] are the rows and columns of scale
  * l; the first num_sink_scales scales are the attention sink (appendix,
@@ -269,12 +299,16 @@ int sparvar_local_blocks(const sparvar_geometry_t* g, int32_t k, int32_t radius,
  *   prev_dilation inside this call (same lists, no extra launch).
  *   row_ptr: int32 [B*H*G_k + 1]; col_idx: int32 [capacity].
  *   radius, prev_dilation: the values the local rows are built with; they
- *   bound the local row length (longer local rows are cut to that bound).
+ *   bound the local row length. A supplied local row longer than that bound
+ *   is cut to it, and the call sets *status (below) to SPARVAR_ERR_CAPACITY.
  *   capacity: >= sparvar_map_index_capacity(...) with the same arguments
  *   (B*H*G_k * M row slots, plus B*H*G_k entries the call uses for row lengths
  *   when a schedule is asked for).
  *   schedule (nullable): int32 [B*H*G_k], the rows ordered longest first,
  *   equal lengths in row order.
+ *   status (nullable): one device int32 that the caller clears beforehand; the
+ *   kernel stores SPARVAR_ERR_CAPACITY there when it cut a supplied local row,
+ *   and writes nothing otherwise (generated local rows always fit).
  * Requires 1 <= S < k <= num_scales.
  */
 int64_t sparvar_map_index_capacity(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t B,
@@ -284,7 +318,7 @@ int sparvar_map_index(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t
                       int32_t topk, const int32_t* topk_idx, const int32_t* local_row_ptr,
                       const int32_t* local_col_idx, int32_t radius, int32_t prev_dilation,
                       int32_t* row_ptr, int32_t* col_idx, int64_t capacity, int32_t* schedule,
-                      hipStream_t stream);
+                      int32_t* status, hipStream_t stream);
 
 /*
  * Index mapping for several target scales in one launch: for each i <
@@ -398,7 +432,11 @@ int sparvar_csla_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t block,
  * made of the kept scales' sides, on which every call above runs unchanged.
  * With the sink scales and the scales that carry CSLA windows kept, the CSLA
  * token mask of the compact schedule is exactly the full mask restricted to the
- * kept tokens (dropped scales hold no kept key).
+ * kept tokens (dropped scales hold no kept key). The 2-D block path is not
+ * served by a compact cache in general: its rows at step k read the sink
+ * scales, scales k - 1 and k (local windows) and every scale the mapping
+ * aligns a selected block to (l + k - S for l <= S, i.e. scales k - S + 1
+ * .. k), which at the Infinity steps is every scale.
  *   keep: host int32 [n_keep], read during the call.
  *   k_src, v_src: [B,H,>= C_{keep[n_keep-1]},d] (plane stride src_bh_stride);
  *   k_dst, v_dst: [B,H,>= sum of N_l over the kept scales,d] (plane stride

@@ -5,7 +5,6 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
-#include <cstdlib>
 #include <cstring>
 
 #include "geometry.h"
@@ -50,10 +49,47 @@ int device_cus() {
   return n;
 }
 
-// Env knobs for launch shape experiments (defaults are the tuned choice).
-int env_int(const char* name, int dflt) {
-  const char* s = std::getenv(name);
-  return s ? std::atoi(s) : dflt;
+// Launch options (sparvar_set_launch_option): process-wide, read at each call.
+// The defaults are the tuned automatic choices.
+constexpr int32_t kOptionDefaults[SPARVAR_OPT_COUNT] = {
+    1,   // SPARVAR_OPT_SWIZZLE
+    0,   // SPARVAR_OPT_DENSE_WAVES
+    64,  // SPARVAR_OPT_DENSE_CHUNK
+    2,   // SPARVAR_OPT_DENSE_STAGES
+    0,   // SPARVAR_OPT_SPARSE_WAVES
+    32,  // SPARVAR_OPT_SPARSE_CHUNK
+    2,   // SPARVAR_OPT_SPARSE_STAGES
+    -1,  // SPARVAR_OPT_SPARSE_GROUP_WAVES
+    64,  // SPARVAR_OPT_SPARSE_GROUP_CHUNK
+    2,   // SPARVAR_OPT_SPARSE_GROUP_STAGES
+    32,  // SPARVAR_OPT_CSLA_CHUNK
+    2,   // SPARVAR_OPT_CSLA_STAGES
+    -1,  // SPARVAR_OPT_CS4A_CHUNK
+    -1,  // SPARVAR_OPT_DECISION_FUSED
+};
+
+std::atomic<int32_t> g_options[SPARVAR_OPT_COUNT] = {
+    kOptionDefaults[0], kOptionDefaults[1], kOptionDefaults[2],  kOptionDefaults[3],  kOptionDefaults[4],
+    kOptionDefaults[5], kOptionDefaults[6], kOptionDefaults[7],  kOptionDefaults[8],  kOptionDefaults[9],
+    kOptionDefaults[10], kOptionDefaults[11], kOptionDefaults[12], kOptionDefaults[13]};
+static_assert(SPARVAR_OPT_COUNT == 14, "one default and one slot per launch option");
+
+int32_t opt(sparvar_launch_option_t o) { return g_options[o].load(std::memory_order_relaxed); }
+
+// softmax_scale must be finite and positive: the bf16 kernels take the running
+// maximum of the raw scores and scale it afterwards.
+int check_softmax_scale(float s) {
+  if (!std::isfinite(s) || !(s > 0.f)) return fail(SPARVAR_ERR_INVALID, "softmax_scale %g is not finite and > 0", s);
+  return SPARVAR_OK;
+}
+
+// The bf16 HBM -> LDS copies address a (b, h) plane of K/V with 32-bit byte
+// offsets: every key row must start below 2^32 bytes into its plane.
+int check_kv_offsets(int64_t n_kv, int32_t d, int elem) {
+  if (elem == 2 && n_kv * d * elem >= (int64_t(1) << 32))
+    return fail(SPARVAR_ERR_INVALID, "K/V plane of %lld tokens x %d exceeds 2^32 bytes (bf16 copy offsets are 32-bit)",
+                (long long)n_kv, d);
+  return SPARVAR_OK;
 }
 
 int build_table(const sparvar_geometry_t* g, GeoTable* T) {
@@ -123,6 +159,17 @@ int32_t local_max_len(const GeoTable& T, int k, int32_t r, int32_t dil, int64_t*
   return mx;
 }
 
+// Limits of the selection kernels (sparvar_select_blocks; the two-call form of
+// sparvar_decision_step): the top-k kernel holds a row of NB scores and ids in
+// 64 KiB of LDS, and the scoring kernel serves query tiles of at most 256 tokens.
+int check_select_limits(const GeoTable& T, int S, bool scoring) {
+  const int32_t NB = T.NB[S];
+  if ((int64_t)NB * 8 > 64 * 1024) return fail(SPARVAR_ERR_UNSUPPORTED, "%d candidate blocks exceed the selection kernel's LDS", NB);
+  if (scoring && T.eh[S - 1] * T.ew[S - 1] > 256)
+    return fail(SPARVAR_ERR_UNSUPPORTED, "query tiles above 256 tokens are not supported by the scoring kernel");
+  return SPARVAR_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -139,6 +186,19 @@ const char* sparvar_status_string(int status) {
 }
 
 const char* sparvar_last_error(void) { return g_last_error; }
+
+int sparvar_set_launch_option(int32_t option, int32_t value) {
+  if (option < 0 || option >= SPARVAR_OPT_COUNT) return fail(SPARVAR_ERR_INVALID, "launch option %d unknown", option);
+  g_options[option].store(value == SPARVAR_OPT_DEFAULT ? kOptionDefaults[option] : value, std::memory_order_relaxed);
+  return ok();
+}
+
+int sparvar_get_launch_option(int32_t option, int32_t* value) {
+  if (option < 0 || option >= SPARVAR_OPT_COUNT) return fail(SPARVAR_ERR_INVALID, "launch option %d unknown", option);
+  if (!value) return fail(SPARVAR_ERR_INVALID, "value is NULL");
+  *value = g_options[option].load(std::memory_order_relaxed);
+  return ok();
+}
 
 int sparvar_scale_info(const sparvar_geometry_t* g, int32_t l, sparvar_scale_info_t* out) {
   GeoTable T;
@@ -168,11 +228,12 @@ int sparvar_dense_attn_fwd(int32_t B, int32_t H, int32_t n_q, int32_t n_kv, int3
   if (st) return st;
   if (B < 1 || H < 1 || n_q < 1 || n_kv < 1) return fail(SPARVAR_ERR_INVALID, "B, H, n_q, n_kv must be >= 1");
   if ((int64_t)B * H * n_q >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "B*H*n_q too large");
-  if (!(std::isfinite(softmax_scale))) return fail(SPARVAR_ERR_INVALID, "softmax_scale is not finite");
+  if ((st = check_softmax_scale(softmax_scale))) return st;
   const int elem = dtype == SPARVAR_BF16 ? 2 : 4;
   if ((st = check_plane(q, q_bh_stride, n_q, d, elem, "q"))) return st;
   if ((st = check_plane(k, kv_bh_stride, n_kv, d, elem, "k"))) return st;
   if ((st = check_plane(v, kv_bh_stride, n_kv, d, elem, "v"))) return st;
+  if ((st = check_kv_offsets(n_kv, d, elem))) return st;
   if ((st = check_plane(o, (int64_t)n_q * d, n_q, d, elem, "o"))) return st;
   DenseAttnArgs a;
   a.BH = B * H;
@@ -188,10 +249,10 @@ int sparvar_dense_attn_fwd(int32_t B, int32_t H, int32_t n_q, int32_t n_kv, int3
   a.q_bh_stride = q_bh_stride;
   a.kv_bh_stride = kv_bh_stride;
   a.softmax_scale = softmax_scale;
-  a.waves = env_int("SPARVAR_DENSE_WAVES", 0);
-  a.chunk = env_int("SPARVAR_DENSE_CHUNK", 64);
-  a.stages = env_int("SPARVAR_DENSE_STAGES", 2);
-  a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
+  a.waves = opt(SPARVAR_OPT_DENSE_WAVES);
+  a.chunk = opt(SPARVAR_OPT_DENSE_CHUNK);
+  a.stages = opt(SPARVAR_OPT_DENSE_STAGES);
+  a.swizzle = opt(SPARVAR_OPT_SWIZZLE);
   a.num_cu = device_cus();
   return hip_status(launch_dense_attn(a, stream), "dense attention launch");
 }
@@ -210,21 +271,20 @@ int sparvar_select_blocks(const sparvar_geometry_t* g, int32_t S, int32_t B, int
   if (topk < 1 || topk > 1024) return fail(SPARVAR_ERR_INVALID, "topk %d outside [1, 1024]", topk);
   if (!topk_idx) return fail(SPARVAR_ERR_INVALID, "topk_idx is NULL");
   const int32_t NB = T.NB[S];
-  if ((int64_t)NB * 8 > 64 * 1024) return fail(SPARVAR_ERR_UNSUPPORTED, "%d candidate blocks exceed the selection kernel's LDS", NB);
+  if ((st = check_select_limits(T, S, !scores_in))) return st;
   const int64_t rows = (int64_t)B * H * tiles_of(T, S);
   if (rows * (NB > topk ? NB : topk) >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "score tensor too large");
   const float* sel_in = scores_in;
   if (!scores_in) {
     if (!scores_out) return fail(SPARVAR_ERR_INVALID, "scores_out is required when scores_in is NULL");
     if ((st = check_dtype_d(dtype, d))) return st;
-    if (T.eh[S - 1] * T.ew[S - 1] > 256)
-      return fail(SPARVAR_ERR_UNSUPPORTED, "query tiles above 256 tokens are not supported by the scoring kernel");
     if (!lse_S) return fail(SPARVAR_ERR_INVALID, "lse_S is NULL");
-    if (!(std::isfinite(softmax_scale))) return fail(SPARVAR_ERR_INVALID, "softmax_scale is not finite");
+    if ((st = check_softmax_scale(softmax_scale))) return st;
     const int elem = dtype == SPARVAR_BF16 ? 2 : 4;
     const int32_t NS = T.h[S - 1] * T.w[S - 1];
     if ((st = check_plane(q_S, q_bh_stride, NS, d, elem, "q_S"))) return st;
     if ((st = check_plane(k_leS, k_bh_stride, T.C[S], d, elem, "k_leS"))) return st;
+    if ((st = check_kv_offsets(T.C[S], d, elem))) return st;
     ScoreArgs a;
     a.G = &T;
     a.S = S;
@@ -258,13 +318,14 @@ int sparvar_decision_step(const sparvar_geometry_t* g, int32_t S, int32_t B, int
   if ((st = check_dtype_d(dtype, d))) return st;
   if (topk < 1 || topk > 1024) return fail(SPARVAR_ERR_INVALID, "topk %d outside [1, 1024]", topk);
   if (!lse_S || !scores_out || !topk_idx) return fail(SPARVAR_ERR_INVALID, "lse_S, scores_out and topk_idx are required");
-  if (!(std::isfinite(softmax_scale))) return fail(SPARVAR_ERR_INVALID, "softmax_scale is not finite");
+  if ((st = check_softmax_scale(softmax_scale))) return st;
   const int elem = dtype == SPARVAR_BF16 ? 2 : 4;
   const int32_t NS = T.h[S - 1] * T.w[S - 1];
   const int32_t NB = T.NB[S];
   if ((st = check_plane(q_S, q_bh_stride, NS, d, elem, "q_S"))) return st;
   if ((st = check_plane(k_leS, kv_bh_stride, T.C[S], d, elem, "k_leS"))) return st;
   if ((st = check_plane(v_leS, kv_bh_stride, T.C[S], d, elem, "v_leS"))) return st;
+  if ((st = check_kv_offsets(T.C[S], d, elem))) return st;
   if ((st = check_plane(o_S, (int64_t)NS * d, NS, d, elem, "o_S"))) return st;
   const int64_t rows = (int64_t)B * H * tiles_of(T, S);
   if ((int64_t)B * H * NS >= (int64_t(1) << 31) || rows * (NB > topk ? NB : topk) >= (int64_t(1) << 31))
@@ -273,7 +334,7 @@ int sparvar_decision_step(const sparvar_geometry_t* g, int32_t S, int32_t B, int
   // room for only one workgroup per CU (many candidate blocks), the two-call
   // sequence is faster. SPARVAR_DECISION_FUSED: 1 = whenever supported, 0 = never.
   size_t lds = 0;
-  const int fused = env_int("SPARVAR_DECISION_FUSED", -1);
+  const int fused = opt(SPARVAR_OPT_DECISION_FUSED);
   const bool can_fuse = dtype == SPARVAR_BF16 && decision_supported(T, S, d, NB, &lds);
   if (can_fuse && (fused == 1 || (fused < 0 && lds <= 80 * 1024))) {
     DecisionArgs a;
@@ -292,9 +353,11 @@ int sparvar_decision_step(const sparvar_geometry_t* g, int32_t S, int32_t B, int
     a.scores = scores_out;
     a.topk = topk;
     a.topk_idx = topk_idx;
-    a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
+    a.swizzle = opt(SPARVAR_OPT_SWIZZLE);
     return hip_status(launch_decision(a, stream), "decision step launch");
   }
+  // the two-call sequence: every limit of both calls is checked before the first enqueues work
+  if ((st = check_select_limits(T, S, true))) return st;
   if ((st = sparvar_dense_attn_fwd(B, H, NS, T.C[S], d, dtype, q_S, q_bh_stride, k_leS, v_leS, kv_bh_stride, o_S,
                                    lse_S, softmax_scale, stream)))
     return st;
@@ -323,10 +386,11 @@ int sparvar_cs4a_column_sums(const sparvar_geometry_t* g, int32_t S, int32_t C, 
   if (dtype != SPARVAR_BF16) return fail(SPARVAR_ERR_UNSUPPORTED, "token-granular paths take bf16 inputs");
   if ((st = check_query_block(C))) return st;
   if (!lse_S || !colsum) return fail(SPARVAR_ERR_INVALID, "lse_S and colsum are required");
-  if (!(std::isfinite(softmax_scale))) return fail(SPARVAR_ERR_INVALID, "softmax_scale is not finite");
+  if ((st = check_softmax_scale(softmax_scale))) return st;
   const int32_t NS = T.h[S - 1] * T.w[S - 1];
   if ((st = check_plane(q_S, q_bh_stride, NS, d, 2, "q_S"))) return st;
   if ((st = check_plane(k_leS, k_bh_stride, T.C[S], d, 2, "k_leS"))) return st;
+  if ((st = check_kv_offsets(T.C[S], d, 2))) return st;
   const int64_t G = (NS + C - 1) / C;
   if ((int64_t)B * H * G * T.C[S] >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "column-sum tensor too large");
   Cs4aColsumArgs a;
@@ -342,7 +406,7 @@ int sparvar_cs4a_column_sums(const sparvar_geometry_t* g, int32_t S, int32_t C, 
   a.q_bh_stride = q_bh_stride;
   a.k_bh_stride = k_bh_stride;
   a.softmax_scale = softmax_scale;
-  a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
+  a.swizzle = opt(SPARVAR_OPT_SWIZZLE);
   a.num_cu = device_cus();
   return hip_status(launch_cs4a_colsum(a, stream), "column-sum launch");
 }
@@ -398,12 +462,13 @@ int sparvar_cs4a_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t C, int
   if ((st = check_query_block(C))) return st;
   if (!tokens || M < 1) return fail(SPARVAR_ERR_INVALID, "tokens and a row stride >= 1 are required");
   if (mode < 0 || mode > 2) return fail(SPARVAR_ERR_INVALID, "mode %d is not 0, 1 or 2", mode);
-  if (!(std::isfinite(softmax_scale))) return fail(SPARVAR_ERR_INVALID, "softmax_scale is not finite");
+  if ((st = check_softmax_scale(softmax_scale))) return st;
   const int32_t Nk = T.h[k - 1] * T.w[k - 1];
   if ((int64_t)B * H * Nk >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "B*H*N_k too large");
   if ((st = check_plane(q_k, q_bh_stride, Nk, d, 2, "q_k"))) return st;
   if ((st = check_plane(k_lek, kv_bh_stride, T.C[k], d, 2, "k_lek"))) return st;
   if ((st = check_plane(v_lek, kv_bh_stride, T.C[k], d, 2, "v_lek"))) return st;
+  if ((st = check_kv_offsets(T.C[k], d, 2))) return st;
   if ((st = check_plane(o, (int64_t)Nk * d, Nk, d, 2, "o"))) return st;
   const int64_t Gk = (Nk + C - 1) / C;
   if ((int64_t)B * H * Gk * M >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "token rows too large");
@@ -437,8 +502,8 @@ int sparvar_cs4a_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t C, int
   a.tokens = tokens;
   a.epi_mode = mode;
   a.epi_base = mode == 0 ? nullptr : base;
-  a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
-  a.chunk = env_int("SPARVAR_CS4A_CHUNK", -1);
+  a.swizzle = opt(SPARVAR_OPT_SWIZZLE);
+  a.chunk = opt(SPARVAR_OPT_CS4A_CHUNK);
   a.num_cu = device_cus();
   return hip_status(launch_token_attn(a, stream), "token attention launch");
 }
@@ -492,12 +557,13 @@ int sparvar_csla_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t block,
   if ((st = check_dtype_d(dtype, d))) return st;
   if (dtype != SPARVAR_BF16) return fail(SPARVAR_ERR_UNSUPPORTED, "the CSLA block path takes bf16 inputs");
   if (!rows || M < 1) return fail(SPARVAR_ERR_INVALID, "rows and a row stride >= 1 are required");
-  if (!(std::isfinite(softmax_scale))) return fail(SPARVAR_ERR_INVALID, "softmax_scale is not finite");
+  if ((st = check_softmax_scale(softmax_scale))) return st;
   const int32_t Nk = T.h[k - 1] * T.w[k - 1];
   if ((int64_t)B * H * Nk >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "B*H*N_k too large");
   if ((st = check_plane(q_k, q_bh_stride, Nk, d, 2, "q_k"))) return st;
   if ((st = check_plane(k_lek, kv_bh_stride, T.C[k], d, 2, "k_lek"))) return st;
   if ((st = check_plane(v_lek, kv_bh_stride, T.C[k], d, 2, "v_lek"))) return st;
+  if ((st = check_kv_offsets(T.C[k], d, 2))) return st;
   if ((st = check_plane(o, (int64_t)Nk * d, Nk, d, 2, "o"))) return st;
   const int64_t Gk = (Nk + block - 1) / block;
   if (Gk * M >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "block rows too large");
@@ -519,9 +585,9 @@ int sparvar_csla_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t block,
   a.block_rows = rows;
   // 32-key chunks in two stages (d = 128): three 4-wave or four 2-wave
   // workgroups per CU; 2-5% ahead of three stages at blocks of 64 and 128
-  a.chunk = env_int("SPARVAR_CSLA_CHUNK", 32);
-  a.stages = env_int("SPARVAR_CSLA_STAGES", 2);
-  a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
+  a.chunk = opt(SPARVAR_OPT_CSLA_CHUNK);
+  a.stages = opt(SPARVAR_OPT_CSLA_STAGES);
+  a.swizzle = opt(SPARVAR_OPT_SWIZZLE);
   return hip_status(launch_block_row_attn(a, stream), "CSLA attention launch");
 }
 
@@ -614,7 +680,7 @@ int sparvar_map_index(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t
                       int32_t topk, const int32_t* topk_idx, const int32_t* local_row_ptr,
                       const int32_t* local_col_idx, int32_t radius, int32_t prev_dilation,
                       int32_t* row_ptr, int32_t* col_idx, int64_t capacity, int32_t* schedule,
-                      hipStream_t stream) {
+                      int32_t* status, hipStream_t stream) {
   GeoTable T;
   int st = build_table(g, &T);
   if (st) return st;
@@ -641,6 +707,7 @@ int sparvar_map_index(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t
   sa.local_col_idx = local_col_idx;
   sa.row_ptr = row_ptr;
   sa.col_idx = col_idx;
+  sa.status = local_row_ptr ? status : nullptr;
   return hip_status(launch_map_index(T, S, B * H, topk, topk_idx, radius, prev_dilation, 1, &sa, schedule, stream),
                     "map index launch");
 }
@@ -683,13 +750,14 @@ int sparvar_map_index_steps(const sparvar_geometry_t* g, int32_t S, int32_t n_st
     sa[i].local_col_idx = nullptr;
     sa[i].row_ptr = row_ptrs[i];
     sa[i].col_idx = col_idxs[i];
+    sa[i].status = nullptr;
   }
   if (blocks >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "too many rows for one launch");
   st = hip_status(launch_map_index(T, S, B * H, topk, topk_idx, radius, prev_dilation, n_steps, sa, nullptr, stream),
                   "map index launch");
   if (st || !orders) return st;
   return hip_status(launch_map_order(T, B * H, topk, n_steps, sa, orders, device_cus(),
-                                     env_int("SPARVAR_SPARSE_GROUP_WAVES", -1), stream),
+                                     opt(SPARVAR_OPT_SPARSE_GROUP_WAVES), stream),
                     "launch order launch");
 }
 
@@ -707,13 +775,14 @@ int sparvar_block_sparse_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_
   if (k < 1 || k > T.L) return fail(SPARVAR_ERR_INVALID, "scale %d outside [1, %d]", k, T.L);
   if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
   if (!row_ptr || !col_idx) return fail(SPARVAR_ERR_INVALID, "row_ptr/col_idx is NULL");
-  if (!(std::isfinite(softmax_scale))) return fail(SPARVAR_ERR_INVALID, "softmax_scale is not finite");
+  if ((st = check_softmax_scale(softmax_scale))) return st;
   const int32_t Nk = T.h[k - 1] * T.w[k - 1];
   if ((int64_t)B * H * Nk >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "B*H*N_k too large");
   const int elem = dtype == SPARVAR_BF16 ? 2 : 4;
   if ((st = check_plane(q_k, q_bh_stride, Nk, d, elem, "q_k"))) return st;
   if ((st = check_plane(k_lek, kv_bh_stride, T.C[k], d, elem, "k_lek"))) return st;
   if ((st = check_plane(v_lek, kv_bh_stride, T.C[k], d, elem, "v_lek"))) return st;
+  if ((st = check_kv_offsets(T.C[k], d, elem))) return st;
   if ((st = check_plane(o, (int64_t)Nk * d, Nk, d, elem, "o"))) return st;
   SparseAttnArgs a;
   a.G = &T;
@@ -732,13 +801,13 @@ int sparvar_block_sparse_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_
   a.row_ptr = row_ptr;
   a.col_idx = col_idx;
   a.schedule = schedule;
-  a.waves = env_int("SPARVAR_SPARSE_WAVES", 0);
-  a.chunk = env_int("SPARVAR_SPARSE_CHUNK", 32);
-  a.stages = env_int("SPARVAR_SPARSE_STAGES", 2);
-  a.swizzle = env_int("SPARVAR_SWIZZLE", 1);
-  a.group_waves = env_int("SPARVAR_SPARSE_GROUP_WAVES", -1);
-  a.group_chunk = env_int("SPARVAR_SPARSE_GROUP_CHUNK", 64);
-  a.group_stages = env_int("SPARVAR_SPARSE_GROUP_STAGES", 2);
+  a.waves = opt(SPARVAR_OPT_SPARSE_WAVES);
+  a.chunk = opt(SPARVAR_OPT_SPARSE_CHUNK);
+  a.stages = opt(SPARVAR_OPT_SPARSE_STAGES);
+  a.swizzle = opt(SPARVAR_OPT_SWIZZLE);
+  a.group_waves = opt(SPARVAR_OPT_SPARSE_GROUP_WAVES);
+  a.group_chunk = opt(SPARVAR_OPT_SPARSE_GROUP_CHUNK);
+  a.group_stages = opt(SPARVAR_OPT_SPARSE_GROUP_STAGES);
   a.num_cu = device_cus();
   return hip_status(launch_sparse_attn(a, stream), "block-sparse attention launch");
 }

@@ -18,6 +18,7 @@
 // same accumulator layout and a simpler register-staged V.
 #include <type_traits>
 
+#include "attn_chunk.h"
 #include "device_common.h"
 #include "launch.h"
 
@@ -891,28 +892,10 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
     ld_row[j] = slot / U;
     ld_unit[j] = (slot % U) ^ (unit_swizzle(ld_row[j]) & (U - 1));
   }
-  // K fragment reads: key row r = 32 kt + l32, logical unit 2 s + half.
-  int k_off[KC / 32][D / 16];
-#pragma unroll
-  for (int kt = 0; kt < KC / 32; ++kt) {
-    const int r = 32 * kt + l32;
-#pragma unroll
-    for (int s2 = 0; s2 < D / 16; ++s2) k_off[kt][s2] = r * kRow + 16 * ((2 * s2 + half) ^ (unit_swizzle(r) & (U - 1)));
-  }
-  // V^T fragment reads through the transposing LDS read: within each group of 16
-  // lanes, lane j receives element t of its 4-element result from the 8-byte
-  // piece addressed by lane 4t + j/4 of the group, at position j % 4. Part p
-  // covers keys 16 ks + 4 half + 8 p + (0..3); the swizzle term does not depend on ks.
-  const int tr_g = lane >> 4, tr_t = (lane & 15) >> 2, tr_q = lane & 3;
-  int v_off[2][D / 32];
-#pragma unroll
-  for (int p = 0; p < 2; ++p) {
-    const int key = 4 * half + 8 * p + tr_t;
-#pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt)
-      v_off[p][dt] = kTile + key * kRow +
-                     16 * ((4 * dt + 2 * (tr_g & 1) + (tr_q >> 1)) ^ (unit_swizzle(key) & (U - 1))) + (tr_q & 1) * 8;
-  }
+  // MFMA fragment offsets: K rows 32 kt + l32 (key tile kt is an immediate
+  // 32 kt rows further) and V^T pieces through the transposing LDS read.
+  FragOffsets<D, KC> fo;
+  fo.init(l32, half, lane);
 
   // Direct loads of a chunk into LDS stage S: 32-bit unsigned byte offsets from the
   // scalar plane bases, wave-uniform LDS destinations.
@@ -994,7 +977,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
     if constexpr (kHoist) {
       if (active) {
 #pragma unroll
-        for (int s2 = 0; s2 < D / 16; ++s2) kf[s2] = *reinterpret_cast<const u32x4*>(kst + k_off[0][s2]);
+        for (int s2 = 0; s2 < D / 16; ++s2) kf[s2] = *reinterpret_cast<const u32x4*>(kst + fo.k_off[s2]);
       }
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -1016,8 +999,8 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
       for (int ks = 0; ks < KC / 16; ++ks)
 #pragma unroll
         for (int dt = 0; dt < D / 32; ++dt) {
-          vlo[ks][dt] = lds_read_tr(kst + v_off[0][dt] + ks * 16 * kRow);
-          vhi[ks][dt] = lds_read_tr(kst + v_off[1][dt] + ks * 16 * kRow);
+          vlo[ks][dt] = lds_read_tr(kst + fo.v_off[0][dt] + ks * 16 * kRow);
+          vhi[ks][dt] = lds_read_tr(kst + fo.v_off[1][dt] + ks * 16 * kRow);
         }
       __builtin_amdgcn_sched_barrier(0);
     } else {
@@ -1025,7 +1008,7 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
       for (int s2 = 0; s2 < D / 16; ++s2) {
 #pragma unroll
         for (int kt = 0; kt < KC / 32; ++kt) {
-          const u32x4 a = *reinterpret_cast<const u32x4*>(kst + k_off[kt][s2]);
+          const u32x4 a = *reinterpret_cast<const u32x4*>(kst + fo.k_off[s2] + kt * 32 * kRow);
           st[kt] = mfma_bf16(as_bf16x8(a), qf.f[s2], st[kt]);
         }
       }
@@ -1080,8 +1063,8 @@ __global__ __launch_bounds__(NW * 64) void attn_bf16_kernel(AttnIO io, Src src) 
           lo = vlo[ks][dt];
           hi = vhi[ks][dt];
         } else {
-          lo = lds_read_tr(kst + v_off[0][dt] + ks * 16 * kRow);
-          hi = lds_read_tr(kst + v_off[1][dt] + ks * 16 * kRow);
+          lo = lds_read_tr(kst + fo.v_off[0][dt] + ks * 16 * kRow);
+          hi = lds_read_tr(kst + fo.v_off[1][dt] + ks * 16 * kRow);
         }
         u32x4 av;
         av[0] = __builtin_bit_cast(uint32_t, __builtin_shufflevector(lo, lo, 0, 1));

@@ -110,6 +110,56 @@ SV_HD void footprint(int32_t a, int32_t e_k, int32_t n_k, int32_t n_p, int32_t e
   *hi = t1 > T_p - 1 ? T_p - 1 : t1;
 }
 
+// Covering form of Decompose-Align-Project (appendix, Spatial Projection applied
+// token by token): the tile's tokens [x0, x1) of scale l span
+// [x0 h_l'/h_l, x1 h_l'/h_l) on scale l' = k - (S - l), and every scale-l' tile
+// overlapping that span (along both axes) is mapped: the box [r0, r1] x [c0, c1]
+// of tiles of scale l'. The span is the footprint above, taken upwards.
+struct CoverBox {
+  int32_t base, Tw;    // first block id of scale l', tiles per row of scale l'
+  int32_t r0, r1, c0, c1;
+};
+
+SV_HD CoverBox map_block_cover(const GeoTable& G, int32_t v, int S, int k) {
+  const int l = block_scale(G, v);
+  const int lp = k - (S - l);
+  const int32_t t = v - G.NB[l - 1];
+  const int32_t tu = t / G.Tw[l - 1], tv = t % G.Tw[l - 1];
+  CoverBox b;
+  b.base = G.NB[lp - 1];
+  b.Tw = G.Tw[lp - 1];
+  footprint(tu, G.eh[l - 1], G.h[l - 1], G.h[lp - 1], G.eh[lp - 1], G.Th[lp - 1], 0, &b.r0, &b.r1);
+  footprint(tv, G.ew[l - 1], G.w[l - 1], G.w[lp - 1], G.ew[lp - 1], G.Tw[lp - 1], 0, &b.c0, &b.c1);
+  return b;
+}
+
+SV_HD int32_t cover_size(const CoverBox& b) { return (b.r1 - b.r0 + 1) * (b.c1 - b.c0 + 1); }
+
+// i-th block (ascending) of a cover box, i < cover_size(b).
+SV_HD int32_t cover_entry(const CoverBox& b, int32_t i) {
+  const int32_t wc = b.c1 - b.c0 + 1;
+  return b.base + (b.r0 + i / wc) * b.Tw + b.c0 + i % wc;
+}
+
+// Largest cover box of any block of scales 1..S mapped to step k (host).
+inline int32_t max_cover_size(const GeoTable& G, int S, int k) {
+  int32_t mx = 1;
+  for (int l = 1; l <= S; ++l) {
+    const int lp = k - (S - l);
+    int32_t mr = 0, mc = 0, lo, hi;
+    for (int32_t t = 0; t < G.Th[l - 1]; ++t) {
+      footprint(t, G.eh[l - 1], G.h[l - 1], G.h[lp - 1], G.eh[lp - 1], G.Th[lp - 1], 0, &lo, &hi);
+      mr = hi - lo + 1 > mr ? hi - lo + 1 : mr;
+    }
+    for (int32_t t = 0; t < G.Tw[l - 1]; ++t) {
+      footprint(t, G.ew[l - 1], G.w[l - 1], G.w[lp - 1], G.ew[lp - 1], G.Tw[lp - 1], 0, &lo, &hi);
+      mc = hi - lo + 1 > mc ? hi - lo + 1 : mc;
+    }
+    mx = mr * mc > mx ? mr * mc : mx;
+  }
+  return mx;
+}
+
 // Parts of local row g of scale k (block form of the CSLA window):
 // [0, n_sink_blocks) sinks; scale-(k-1) footprint tiles; scale-k window tiles.
 struct LocalRow {

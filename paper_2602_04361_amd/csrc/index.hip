@@ -12,6 +12,7 @@
 // schedule_kernel (optional): the rows' longest-first stable order.
 #include "device_common.h"
 #include "launch.h"
+#include "sparvar.h"
 
 namespace sparvar {
 
@@ -65,6 +66,7 @@ struct MapStep {
   int32_t* row_ptr;
   int32_t* col_idx;
   int32_t* counts;  // [rows] row lengths
+  int32_t* status;  // nullable: receives kStatusCut when a supplied local row is cut
   int32_t k, G_k, rows, max_cand, block0;
 };
 
@@ -78,6 +80,7 @@ struct MapIO {
 
 constexpr int kMapWaves = 4;
 constexpr int32_t kInvalid = 0x7fffffff;
+constexpr int32_t kStatusCut = SPARVAR_ERR_CAPACITY;
 
 // One wave per row: candidates (local row + mapped selection) in LDS, first
 // occurrences kept, each kept id written at its rank; the row occupies
@@ -120,7 +123,12 @@ __global__ __launch_bounds__(kMapWaves * 64) void map_rows_kernel(MapIO io) {
       n_loc = local_row_len(lr);
     }
     if (n_loc < 0) n_loc = 0;
-    if (n_loc > ms.max_cand - io.topk) n_loc = ms.max_cand - io.topk;
+    if (n_loc > ms.max_cand - io.topk) {
+      // a supplied local row longer than the (radius, dilation) bound: cut to
+      // the bound, and reported through the caller's status word
+      n_loc = ms.max_cand - io.topk;
+      if (ms.status && lane == 0) *ms.status = kStatusCut;
+    }
   }
   const int32_t n = active ? n_loc + io.topk : 0;
   const int32_t* sel = io.topk_idx + ((int64_t)bh * io.G_S + gs) * io.topk;
@@ -324,6 +332,7 @@ hipError_t launch_map_index(const GeoTable& G, int S, int32_t BH, int32_t topk, 
     m.rows = BH * m.G_k;
     m.max_cand = a.max_local + topk;
     m.counts = a.col_idx + (int64_t)m.rows * m.max_cand;  // past the last row slot
+    m.status = a.status;
     m.block0 = blocks;
     blocks += (m.rows + kMapWaves - 1) / kMapWaves;
     max_cand = m.max_cand > max_cand ? m.max_cand : max_cand;

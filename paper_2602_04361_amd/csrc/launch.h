@@ -160,6 +160,7 @@ struct MapStepArgs {
   int32_t k, max_local;
   const int32_t *local_row_ptr, *local_col_idx;  // both NULL: generated
   int32_t *row_ptr, *col_idx;
+  int32_t* status;  // nullable: set to SPARVAR_ERR_CAPACITY when a supplied local row is cut to max_local
 };
 constexpr int kMaxMapSteps = 8;
 // Rows of every listed step in one launch; the schedule (single step only) is

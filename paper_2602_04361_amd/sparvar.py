@@ -7,12 +7,15 @@ call raises: there is no fallback path.
 """
 from __future__ import annotations
 
+import contextlib
 import ctypes
 import math
 import os
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libsparvar.so")
+# SPARVAR_LIBRARY selects another build of the same library (e.g. the
+# host-sanitized one of build_host_sanitized.py); the default is the in-tree build.
+LIB_PATH = os.environ.get("SPARVAR_LIBRARY") or os.path.join(_HERE, "libsparvar.so")
 
 OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_CAPACITY, ERR_HIP = 0, -1, -2, -3, -4
 BF16, F32 = 0, 1
@@ -40,7 +43,15 @@ EXPORTS = [
     "sparvar_block_sparse_attn_fwd",
     "sparvar_status_string",
     "sparvar_last_error",
+    "sparvar_set_launch_option",
+    "sparvar_get_launch_option",
 ]
+
+# sparvar_launch_option_t, in enum order
+LAUNCH_OPTIONS = ["SWIZZLE", "DENSE_WAVES", "DENSE_CHUNK", "DENSE_STAGES", "SPARSE_WAVES", "SPARSE_CHUNK",
+                  "SPARSE_STAGES", "SPARSE_GROUP_WAVES", "SPARSE_GROUP_CHUNK", "SPARSE_GROUP_STAGES", "CSLA_CHUNK",
+                  "CSLA_STAGES", "CS4A_CHUNK", "DECISION_FUSED"]
+OPT_DEFAULT = -(1 << 31)
 
 
 class SparvarError(RuntimeError):
@@ -103,11 +114,14 @@ def load_library(path: str = LIB_PATH):
         "sparvar_local_blocks_capacity": (i64, [G, i32, i32, i32]),
         "sparvar_local_blocks": (ctypes.c_int, [G, i32, i32, i32, vp, vp, i64, vp]),
         "sparvar_map_index_capacity": (i64, [G, i32, i32, i32, i32, i32, i32, i32]),
-        "sparvar_map_index": (ctypes.c_int, [G, i32, i32, i32, i32, i32, vp, vp, vp, i32, i32, vp, vp, i64, vp, vp]),
+        "sparvar_map_index": (ctypes.c_int, [G, i32, i32, i32, i32, i32, vp, vp, vp, i32, i32, vp, vp, i64, vp, vp,
+                                             vp]),
         "sparvar_block_sparse_attn_fwd": (ctypes.c_int, [G, i32, i32, i32, i32, ctypes.c_int, vp, i64, vp, vp, i64,
                                                          vp, vp, f32, vp, vp, vp, vp]),
         "sparvar_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "sparvar_last_error": (ctypes.c_char_p, []),
+        "sparvar_set_launch_option": (ctypes.c_int, [i32, i32]),
+        "sparvar_get_launch_option": (ctypes.c_int, [i32, ctypes.POINTER(ctypes.c_int32)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(lib, name)
@@ -144,6 +158,31 @@ class Geometry:
         info = _CScaleInfo()
         _check(load_library().sparvar_scale_info(self.ref, int(l), ctypes.byref(info)))
         return {n: getattr(info, n) for n, _ in _CScaleInfo._fields_}
+
+
+def sparvar_set_launch_option(name, value=None):
+    """Set launch option `name` (a LAUNCH_OPTIONS entry) process-wide; None restores its default."""
+    _check(load_library().sparvar_set_launch_option(LAUNCH_OPTIONS.index(name),
+                                                    OPT_DEFAULT if value is None else int(value)))
+
+
+def sparvar_get_launch_option(name):
+    v = ctypes.c_int32()
+    _check(load_library().sparvar_get_launch_option(LAUNCH_OPTIONS.index(name), ctypes.byref(v)))
+    return v.value
+
+
+@contextlib.contextmanager
+def launch_options(**opts):
+    """Set launch options for the body of a with-statement, then restore the previous values."""
+    before = {n: sparvar_get_launch_option(n) for n in opts}
+    try:
+        for n, v in opts.items():
+            sparvar_set_launch_option(n, v)
+        yield
+    finally:
+        for n, v in before.items():
+            sparvar_set_launch_option(n, v)
 
 
 # ---------------------------------------------------------------- tensor helpers
@@ -354,11 +393,13 @@ def sparvar_map_index_capacity(geom, S, k, B, H, topk, radius, prev_dilation=0):
 
 
 def sparvar_map_index(geom, S, k, B, H, topk, topk_idx, local_row_ptr, local_col_idx, radius, row_ptr, col_idx,
-                      schedule=None, prev_dilation=0, stream=None):
-    """Mapped + local blocks -> CSR; local_row_ptr/local_col_idx may both be None."""
+                      schedule=None, prev_dilation=0, status=None, stream=None):
+    """Mapped + local blocks -> CSR; local_row_ptr/local_col_idx may both be None. status (optional one-element
+    int32 device tensor, cleared by the caller) receives ERR_CAPACITY if a supplied local row was cut."""
     _check(load_library().sparvar_map_index(geom.ref, S, k, B, H, topk, _ptr(topk_idx), _ptr(local_row_ptr),
                                             _ptr(local_col_idx), radius, prev_dilation, _ptr(row_ptr),
-                                            _ptr(col_idx), col_idx.numel(), _ptr(schedule), _stream(stream)))
+                                            _ptr(col_idx), col_idx.numel(), _ptr(schedule), _ptr(status),
+                                            _stream(stream)))
     return row_ptr, col_idx, schedule
 
 

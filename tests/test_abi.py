@@ -127,7 +127,7 @@ def test_attention_validation_before_launch():
     assert lib.sparvar_select_blocks(g.ref, 10, 1, 1, 128, sv.BF16, fake, 1024 * 128, fake, 2521 * 128, fake, 0.1,
                                      None, None, 8, fake, None) == sv.ERR_INVALID
     assert lib.sparvar_local_blocks(g.ref, 13, 1, 0, fake, fake, 10, None) == sv.ERR_CAPACITY
-    assert lib.sparvar_map_index(g.ref, 10, 13, 1, 1, 8, fake, fake, fake, 1, 0, fake, fake, 10, None,
+    assert lib.sparvar_map_index(g.ref, 10, 13, 1, 1, 8, fake, fake, fake, 1, 0, fake, fake, 10, None, None,
                                  None) == sv.ERR_CAPACITY
     assert b"capacity" in lib.sparvar_last_error()
 
@@ -232,3 +232,82 @@ def test_kv_compact_validation_before_launch():
     assert call(keep, dst=8120 * 128) == sv.ERR_INVALID    # compact plane too short
     assert call(keep, src=10520 * 128) == sv.ERR_INVALID   # source plane too short for scale 13
     assert sv.compact_geometry(g, keep).h == [1, 2, 4, 6, 8, 40, 48, 64]
+
+
+def test_softmax_scale_must_be_positive():
+    # the bf16 kernels take the running max of the raw scores, so scale <= 0 is refused everywhere
+    lib = sv.load_library()
+    vp = ctypes.c_void_p
+    fake = vp(1 << 20)
+    g = sv.Geometry(INF, INF, 8, 4)
+    for scale in (0.0, -0.1, float("-inf")):
+        assert lib.sparvar_dense_attn_fwd(1, 1, 4, 4, 64, sv.BF16, fake, 256, fake, fake, 256, fake, None, scale,
+                                          None) == sv.ERR_INVALID
+        assert lib.sparvar_block_sparse_attn_fwd(g.ref, 13, 1, 1, 128, sv.BF16, fake, 4096 * 128, fake, fake,
+                                                 10521 * 128, fake, None, scale, fake, fake, None,
+                                                 None) == sv.ERR_INVALID
+        assert lib.sparvar_decision_step(g.ref, 10, 1, 1, 128, sv.BF16, fake, 1024 * 128, fake, fake, 2521 * 128,
+                                         fake, fake, scale, fake, 8, fake, None) == sv.ERR_INVALID
+        assert lib.sparvar_csla_attn_fwd(g.ref, 13, 128, 1, 1, 128, sv.BF16, fake, 4096 * 128, fake, fake,
+                                         10521 * 128, fake, None, scale, fake, 83, None) == sv.ERR_INVALID
+        assert lib.sparvar_select_blocks(g.ref, 10, 1, 1, 128, sv.BF16, fake, 1024 * 128, fake, 2521 * 128, fake,
+                                         scale, None, fake, 8, fake, None) == sv.ERR_INVALID
+        assert b"softmax_scale" in lib.sparvar_last_error()
+
+
+def test_bf16_plane_offsets_limited_to_32_bits():
+    # the bf16 HBM -> LDS copies use 32-bit byte offsets inside a (b, h) plane
+    lib = sv.load_library()
+    vp = ctypes.c_void_p
+    fake = vp(1 << 20)
+    n_kv = 1 << 24  # x 128 x 2 bytes = 2^32
+    assert lib.sparvar_dense_attn_fwd(1, 1, 4, n_kv, 128, sv.BF16, fake, 4 * 128, fake, fake, n_kv * 128, fake,
+                                      None, 0.1, None) == sv.ERR_INVALID
+    assert b"2^32" in lib.sparvar_last_error()
+    side = [1, 4097]  # 16785410 cache tokens at step 2
+    g = sv.Geometry(side, side, 8, 1)
+    nq = 4097 * 4097
+    assert lib.sparvar_block_sparse_attn_fwd(g.ref, 2, 1, 1, 128, sv.BF16, fake, nq * 128, fake, fake,
+                                             (nq + 1) * 128, fake, None, 0.1, fake, fake, None,
+                                             None) == sv.ERR_INVALID
+    assert b"2^32" in lib.sparvar_last_error()
+
+
+def test_decision_step_fallback_validates_before_any_launch():
+    # 32x32-token tiles at the 32x32 decision scale: the fused kernel does not take
+    # them and the scoring kernel of the two-call sequence serves at most 256-token
+    # tiles, so the call must fail before it enqueues the dense attention (on this
+    # GPU-less host an enqueued launch would report a HIP error instead)
+    lib = sv.load_library()
+    vp = ctypes.c_void_p
+    fake = vp(1 << 20)
+    g = sv.Geometry(INF, INF, 32, 4)
+    st = lib.sparvar_decision_step(g.ref, 10, 1, 1, 128, sv.BF16, fake, 1024 * 128, fake, fake, 2521 * 128, fake,
+                                   fake, 0.1, fake, 8, fake, None)
+    assert st == sv.ERR_UNSUPPORTED, lib.sparvar_last_error()
+    assert b"256 tokens" in lib.sparvar_last_error()
+
+
+def test_launch_options_set_get_reset():
+    lib = sv.load_library()
+    defaults = {n: sv.sparvar_get_launch_option(n) for n in sv.LAUNCH_OPTIONS}
+    assert defaults["SWIZZLE"] == 1 and defaults["SPARSE_CHUNK"] == 32 and defaults["SPARSE_GROUP_WAVES"] == -1
+    with sv.launch_options(SPARSE_CHUNK=64, SWIZZLE=0):
+        assert sv.sparvar_get_launch_option("SPARSE_CHUNK") == 64 and sv.sparvar_get_launch_option("SWIZZLE") == 0
+    assert {n: sv.sparvar_get_launch_option(n) for n in sv.LAUNCH_OPTIONS} == defaults
+    sv.sparvar_set_launch_option("DENSE_WAVES", 4)
+    sv.sparvar_set_launch_option("DENSE_WAVES", None)  # back to the default
+    assert sv.sparvar_get_launch_option("DENSE_WAVES") == defaults["DENSE_WAVES"]
+    v = ctypes.c_int32()
+    assert lib.sparvar_set_launch_option(len(sv.LAUNCH_OPTIONS), 1) == sv.ERR_INVALID
+    assert lib.sparvar_get_launch_option(-1, ctypes.byref(v)) == sv.ERR_INVALID
+    assert lib.sparvar_get_launch_option(0, None) == sv.ERR_INVALID
+
+
+def test_launch_option_names_follow_the_header():
+    with open(os.path.join(ROOT, "include", "sparvar.h")) as f:
+        text = f.read()
+    body = text[text.index("typedef enum sparvar_launch_option"):text.index("} sparvar_launch_option_t;")]
+    names = re.findall(r"SPARVAR_OPT_(\w+)", body)
+    assert names[-1] == "COUNT" and names[0] == "SWIZZLE"
+    assert names[:-1] == sv.LAUNCH_OPTIONS

@@ -85,10 +85,10 @@ def test_infinity_layer_full_size_sampled_heads():
 
 @pytest.mark.parametrize("chunk", ["32", "64"])
 @pytest.mark.parametrize("C", [64, 128])
-def test_gather_chunks_of_32_and_64_keys(monkeypatch, chunk, C):
+def test_gather_chunks_of_32_and_64_keys(launch_option, chunk, C):
     # both chunk shapes of the gather attention at d = 128 (two and four waves),
     # for the O_cache pass at S and the later steps
-    monkeypatch.setenv("SPARVAR_CS4A_CHUNK", chunk)
+    launch_option("CS4A_CHUNK", chunk)
     cs4a_case(INF_SIDES, 8, 4, 10, [11, 13], 1, 2, 128, 32, C, 200, 46 + C, heads=[1])
 
 

@@ -1,6 +1,7 @@
 """GPU parity of the CSLA block path (called through the C ABI) against the fp64
 oracle on the same seeded inputs: block rows bit-exact; attention outputs within
-the bf16 tolerance (max-abs 2e-2, mean-abs 2e-3) and LSE within 2e-2."""
+the bf16 tolerance (max-abs 2e-2, mean-abs 2e-3) and LSE within 2e-4, the bar of
+the same attention core on the 2-D block path."""
 import numpy as np
 import pytest
 import torch
@@ -84,7 +85,7 @@ def attn_case(h, ns, k, windows, block, B, H, d, seed, heads=None):
         mx, mean = assert_close(o[bh], ref, "bf16", f"head {bh}")
         fin = np.isfinite(ref_lse)
         assert (np.isneginf(lse[bh]) == ~fin).all()
-        assert np.abs(lse[bh][fin] - ref_lse[fin]).max(initial=0) <= 2e-2
+        assert np.abs(lse[bh][fin] - ref_lse[fin]).max(initial=0) <= 2e-4
     note(f"  ok (last head max {mx:.2e} mean {mean:.2e})")
     return rows
 
@@ -132,10 +133,10 @@ def test_attention_empty_rows_give_zero_and_stop_at_first_invalid_id():
 
 
 @pytest.mark.parametrize("stages", [2, 3, 4])
-def test_attention_chunks_of_32(monkeypatch, stages):
+def test_attention_chunks_of_32(launch_option, stages):
     # the 32-key chunk shapes (d = 128, two to eight waves)
-    monkeypatch.setenv("SPARVAR_CSLA_CHUNK", "32")
-    monkeypatch.setenv("SPARVAR_CSLA_STAGES", str(stages))
+    launch_option("CSLA_CHUNK", "32")
+    launch_option("CSLA_STAGES", str(stages))
     for block in (64, 128, 256):
         attn_case(INF_SIDES[:10], 5, 10, O.default_windows(10), block, 1, 2, 128, 56 + block)
 

@@ -20,10 +20,10 @@ from test_gpu_parity import run_case
 pytestmark = pytest.mark.gpu
 
 FORMS = {
-    "per_tile": {"SPARVAR_SPARSE_GROUP_WAVES": "0"},
-    "group4": {"SPARVAR_SPARSE_GROUP_WAVES": "4"},
-    "group8": {"SPARVAR_SPARSE_GROUP_WAVES": "8"},
-    "group8_kc32": {"SPARVAR_SPARSE_GROUP_WAVES": "8", "SPARVAR_SPARSE_GROUP_CHUNK": "32"},
+    "per_tile": {"SPARSE_GROUP_WAVES": "0"},
+    "group4": {"SPARSE_GROUP_WAVES": "4"},
+    "group8": {"SPARSE_GROUP_WAVES": "8"},
+    "group8_kc32": {"SPARSE_GROUP_WAVES": "8", "SPARSE_GROUP_CHUNK": "32"},
 }
 
 
@@ -45,9 +45,9 @@ def random_rows(nb, n_rows, rng, long_every, long_len, short_len):
     return rows, clean
 
 
-def run_rows(monkeypatch, form, h, w, b, ns, k, B, H, d, seed, long_every, long_len, short_len):
+def run_rows(launch_option, form, h, w, b, ns, k, B, H, d, seed, long_every, long_len, short_len):
     for key, val in FORMS[form].items():
-        monkeypatch.setenv(key, val)
+        launch_option(key, val)
     note(f"[grouped] form={form} h={h} w={w} b={b} k={k} B={B} H={H} d={d} seed={seed}")
     q, kk, v = make_case(h, w, B, H, d, 8, ns, seed, "bf16")
     og = oracle_geometry(h, w, b, ns)
@@ -80,33 +80,33 @@ def run_rows(monkeypatch, form, h, w, b, ns, k, B, H, d, seed, long_every, long_
 
 
 @pytest.mark.parametrize("form", list(FORMS))
-def test_forms_infinity_last_scale(monkeypatch, form):
+def test_forms_infinity_last_scale(launch_option, form):
     # 8x8 tiles at 64x64 (2 waves a tile); every 9th row longer than 128 blocks
-    run_rows(monkeypatch, form, INF_SIDES, INF_SIDES, 8, 4, 13, 1, 2, 128, 21, 9, 140, 40)
+    run_rows(launch_option, form, INF_SIDES, INF_SIDES, 8, 4, 13, 1, 2, 128, 21, 9, 140, 40)
 
 
 @pytest.mark.parametrize("form", ["per_tile", "group4", "group8"])
-def test_forms_small_tiles_partial_groups(monkeypatch, form):
+def test_forms_small_tiles_partial_groups(launch_option, form):
     # 4x4 tiles (16 queries, one wave a tile) on a 27x27 scale: edge tiles 3 wide
     # and groups hanging over the scale's edge; rows of 70 blocks exceed the
     # merge capacity of 64 entries per tile
     h = [1, 2, 3, 5, 7, 10, 13, 20, 27]
-    run_rows(monkeypatch, form, h, h, 4, 2, 9, 1, 2, 64, 22, 7, 70, 20)
+    run_rows(launch_option, form, h, h, 4, 2, 9, 1, 2, 64, 22, 7, 70, 20)
 
 
 @pytest.mark.parametrize("form", ["group4", "group8"])
-def test_forms_nonsquare_d64(monkeypatch, form):
+def test_forms_nonsquare_d64(launch_option, form):
     h = [1, 2, 3, 5, 8, 11, 17]
     w = [1, 3, 4, 7, 9, 14, 21]
-    run_rows(monkeypatch, form, h, w, 8, 2, 7, 2, 2, 64, 23, 0, 0, 12)
+    run_rows(launch_option, form, h, w, 8, 2, 7, 2, 2, 64, 23, 0, 0, 12)
 
 
 @pytest.mark.parametrize("form", ["per_tile", "group4"])
-def test_forms_on_pipeline_rows(monkeypatch, form):
+def test_forms_on_pipeline_rows(launch_option, form):
     # The whole path (decision, mapping, attention at 40/48/64) with the rows the
     # mapping step writes; the automatic form is covered by the parity suite.
     for key, val in FORMS[form].items():
-        monkeypatch.setenv(key, val)
+        launch_option(key, val)
     run_case(INF_SIDES, INF_SIDES, 8, 4, 10, [11, 12, 13], 1, 4, 128, 32, 8, 1, "bf16", seed=12,
              tiles_per_step=16)
 
@@ -133,11 +133,11 @@ def check_order(order, lengths, n_items, grouped, item_len):
 
 
 @pytest.mark.parametrize("form", ["per_tile", "group4"])
-def test_launch_order_from_the_mapping(monkeypatch, form):
+def test_launch_order_from_the_mapping(launch_option, form):
     # one mapping launch writes every step's order; the attention gives the same
     # bits with and without it, and ignores an order of the other form
     for key, val in FORMS[form].items():
-        monkeypatch.setenv(key, val)
+        launch_option(key, val)
     from paper_2602_04361_amd.pipeline import SparsePath
 
     h, b, ns, S, steps, B, H, d = INF_SIDES, 8, 4, 10, [11, 12, 13], 1, 4, 128

@@ -176,11 +176,11 @@ def test_infinity_wide_32_heads_full_size():
              heads=[0, 45, 63], tiles_per_step=8)
 
 
-@pytest.mark.parametrize("b,topk,r", [(8, 4, 2), (8, 32, 1), (16, 4, 1), (16, 32, 2)])
+@pytest.mark.parametrize("b,topk,r", [(b, t, r) for b in (8, 16) for r in (1, 2) for t in (4, 8, 16, 32)])
 def test_sparsity_sweep_settings_full_size(b, topk, r):
-    # the sparsity sweep's settings on the Infinity layer (B=2, H=16, d=128): top-k
-    # 4 and 32, blocks of 8x8 and 16x16 tokens, local radius 1 and 2. Index lists
-    # bit-exact on all heads; attention sampled on two heads.
+    # all 16 settings of the sparsity sweep on the Infinity layer (B=2, H=16,
+    # d=128): top-k 4, 8, 16 and 32, blocks of 8x8 and 16x16 tokens, local radius
+    # 1 and 2. Index lists bit-exact on all heads; attention sampled on two heads.
     run_case(INF_SIDES, INF_SIDES, b, 4, 10, [11, 12, 13], 2, 16, 128, 32, topk, r, "bf16", seed=40 + topk + r,
              heads=[3, 26], tiles_per_step=6)
 
@@ -278,12 +278,12 @@ def test_deterministic_and_schedule_invariant():
 
 
 @pytest.mark.parametrize("group_waves", ["0", "4"])
-def test_full_rows_past_the_chunk_table(monkeypatch, group_waves):
+def test_full_rows_past_the_chunk_table(launch_option, group_waves):
     # every 8x8 tile of the 64x64 scale lists all 172 blocks of the Infinity cache:
     # 344 chunks of 32 keys per row, past the 256-entry chunk table (refills), and
     # for pairs of tiles past the row-merge capacity (served tile by tile); the
     # result is dense attention over the 10521-token cache
-    monkeypatch.setenv("SPARVAR_SPARSE_GROUP_WAVES", group_waves)
+    launch_option("SPARSE_GROUP_WAVES", group_waves)
     h, d = INF_SIDES, 128
     note(f"[parity] full rows at 64x64, group waves {group_waves}")
     g = sv.Geometry(h, h, 8, 4)
