@@ -57,6 +57,8 @@ def parse():
                          "sparsity-sweep workloads (per-layer times, TFLOP/s, density, speedup)")
     ap.add_argument("--csla", action="store_true",
                     help="instead of the step line: the CSLA block-path settings only")
+    ap.add_argument("--only", default=None,
+                    help="with --sweep: only the block-path workloads whose name contains this string")
     return ap.parse_args()
 
 
@@ -194,13 +196,15 @@ def kernel_source_hash():
 
 # ---------------------------------------------------------------- sweep of the other workloads
 SWEEP = ([dict(name="heads32", sides=SIDES, B=2, H=32, b=8, S=10, steps=[11, 12, 13], topk=8, radius=1, sets=4),
+          dict(name="cover_projection", sides=SIDES, B=2, H=16, b=8, S=10, steps=[11, 12, 13], topk=8, radius=1,
+               sets=4, projection="cover"),
           dict(name="schedule2048", sides=SIDES + [80, 96, 128], B=1, H=16, b=8, S=13, steps=[14, 15, 16], topk=16,
                radius=1, sets=2)] +
          [dict(name=f"last_step_b{b}_r{r}_top{t}", sides=SIDES, B=2, H=16, b=b, S=10, steps=[13], topk=t, radius=r,
                sets=4) for b in (8, 16) for r in (1, 2) for t in (4, 8, 16, 32)])
 
 
-def sweep(args, dev):
+def sweep(args, dev, only=None):
     import torch
 
     from paper_2602_04361_amd import sparvar as sv
@@ -210,6 +214,8 @@ def sweep(args, dev):
     d, nf, ns = CFG["d"], CFG["n_freq"], CFG["n_sink"]
     cache = {}
     for st in SWEEP:
+        if only is not None and only not in st["name"]:
+            continue
         key = (tuple(st["sides"]), st["B"], st["H"], st["sets"])
         if key not in cache:
             cache.clear()
@@ -222,7 +228,8 @@ def sweep(args, dev):
         sets = cache[key]
         B, H = st["B"], st["H"]
         g = sv.Geometry(st["sides"], st["sides"], st["b"], ns)
-        path = SparsePath(g, st["S"], st["steps"], B, H, d, st["topk"], st["radius"])
+        path = SparsePath(g, st["S"], st["steps"], B, H, d, st["topk"], st["radius"],
+                          projection=st.get("projection", "point"))
         info = path.info
         stream = torch.cuda.current_stream()
         n_ev = 3 + len(st["steps"])
@@ -252,6 +259,7 @@ def sweep(args, dev):
         torch.cuda.synchronize()
         med = lambda a, b: float(np.median([evs[i][a].elapsed_time(evs[i][b]) for i in range(n)]))
         out = {"sweep": st["name"], "B": B, "H": H, "block": st["b"], "topk": st["topk"], "radius": st["radius"],
+               "projection": st.get("projection", "point"),
                "decision_scale": st["sides"][st["S"] - 1], "decision_ms": med(0, 1),
                "map_all_steps_ms": med(1, 2), "steps": {}}
         BH = B * H
@@ -512,6 +520,9 @@ def main():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
     dev = torch.device("cuda:0")
+    if args.sweep and args.only:
+        sweep(args, dev, only=args.only)
+        return
     if args.sweep:
         sweep(args, dev)
         sweep_cs4a(dev)

@@ -280,19 +280,33 @@ int sparvar_local_blocks(const sparvar_geometry_t* g, int32_t k, int32_t radius,
                          int32_t prev_dilation, int32_t* row_ptr, int32_t* col_idx,
                          int64_t capacity, hipStream_t stream);
 
+/* Projection step of Decompose-Align-Project (appendix, Relative Scale
+ * Alignment, Spatial Projection), at block granularity. */
+typedef enum sparvar_projection {
+  /* the tile origin (x,y) -> (floor(x h_l'/h_l), floor(y w_l'/w_l)), and the
+   * scale-l' tile containing it: one block per selected block */
+  SPARVAR_PROJECT_POINT = 0,
+  /* every scale-l' tile overlapping the upsampled span [x0 h_l'/h_l,
+   * x1 h_l'/h_l) x [y0 w_l'/w_l, y1 w_l'/w_l) of the tile's tokens [x0, x1) x
+   * [y0, y1): a selection keeps its share of its scale's area */
+  SPARVAR_PROJECT_COVER = 1
+} sparvar_projection_t;
+
 /*
  * Cross-scale index mapping and merge into CSR (appendix "Cross-Scale Sparse
  * Index Mapping" and "Attention Sink"). For target query tile (a,c) of scale
  * k and every (b,h): the source tile is the Query Block Homography
  * (floor((2a+1) T_h(S) / (2 T_h(k))), same for c); each selected block of
  * topk_idx[b,h,source,:] (skipping -1) goes through Decompose-Align-Project:
- * scale l -> l' = k - (S - l), tile origin (x,y) -> (floor(x h_l'/h_l),
- * floor(y w_l'/w_l)), and the scale-l' tile containing it. The row is the
- * ascending, duplicate-free union of the mapped blocks and local row (a,c).
- * Row index r = (b*H + h) * G_k + g.
+ * scale l -> l' = k - (S - l), then the projection (sparvar_projection_t).
+ * The row is the ascending, duplicate-free union of the mapped blocks and
+ * local row (a,c). Row index r = (b*H + h) * G_k + g.
  * Output layout (padded CSR): rows have a fixed stride M = (longest local row)
- * + topk: row_ptr[r] = r * M, and col_idx[r*M .. r*M + M) holds the row's ids
- * followed by -1 up to the stride (sparvar_block_sparse_attn_fwd skips them).
+ * + topk * P, with P = 1 for the point projection and P = the largest cover
+ * box of any block of scales 1..S for the covering one (9 at the Infinity
+ * steps 40/48/64 from 32x32): row_ptr[r] = r * M, and col_idx[r*M .. r*M + M)
+ * holds the row's ids followed by -1 up to the stride
+ * (sparvar_block_sparse_attn_fwd skips them).
  *   topk_idx: int32 [B,H,G_S,topk] (from sparvar_select_blocks).
  *   local_row_ptr / local_col_idx: output of sparvar_local_blocks for k, or
  *   both NULL: the local rows are then generated from radius and
@@ -313,25 +327,25 @@ int sparvar_local_blocks(const sparvar_geometry_t* g, int32_t k, int32_t radius,
  */
 int64_t sparvar_map_index_capacity(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t B,
                                    int32_t H, int32_t topk, int32_t radius,
-                                   int32_t prev_dilation); /* upper bound, < 0 on error */
+                                   int32_t prev_dilation, int32_t projection); /* upper bound, < 0 on error */
 int sparvar_map_index(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t B, int32_t H,
                       int32_t topk, const int32_t* topk_idx, const int32_t* local_row_ptr,
                       const int32_t* local_col_idx, int32_t radius, int32_t prev_dilation,
-                      int32_t* row_ptr, int32_t* col_idx, int64_t capacity, int32_t* schedule,
-                      int32_t* status, hipStream_t stream);
+                      int32_t projection, int32_t* row_ptr, int32_t* col_idx, int64_t capacity,
+                      int32_t* schedule, int32_t* status, hipStream_t stream);
 
 /*
  * Index mapping for several target scales in one launch: for each i <
  * n_steps (1 <= n_steps <= 8), the rows of scale ks[i] exactly as
  * sparvar_map_index(g, S, ks[i], B, H, topk, topk_idx, NULL, NULL, radius,
- * prev_dilation, row_ptrs[i], col_idxs[i], capacities[i], NULL, stream) writes
- * them (local rows generated in the call). The mapping of every later scale
+ * prev_dilation, projection, row_ptrs[i], col_idxs[i], capacities[i], NULL,
+ * NULL, stream) writes them (local rows generated in the call). The mapping of every later scale
  * depends only on the selection at S, so all of them can be built right after
  * the decision step.
  *   ks, row_ptrs, col_idxs, capacities: host arrays of n_steps entries, read
  *   during the call; row_ptrs[i], col_idxs[i] are device buffers sized as for
  *   sparvar_map_index, capacities[i] >= sparvar_map_index_capacity(g, S,
- *   ks[i], B, H, topk, radius, prev_dilation).
+ *   ks[i], B, H, topk, radius, prev_dilation, projection).
  *   orders (nullable host array of n_steps nullable device pointers, each
  *   int32 [B*H*G_k of ks[i]]): a launch order for sparvar_block_sparse_attn_fwd
  *   at ks[i] (its schedule argument), written from the row lengths by a second
@@ -344,9 +358,9 @@ int sparvar_map_index(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t
  */
 int sparvar_map_index_steps(const sparvar_geometry_t* g, int32_t S, int32_t n_steps, const int32_t* ks,
                             int32_t B, int32_t H, int32_t topk, const int32_t* topk_idx,
-                            int32_t radius, int32_t prev_dilation, int32_t* const* row_ptrs,
-                            int32_t* const* col_idxs, const int64_t* capacities,
-                            int32_t* const* orders, hipStream_t stream);
+                            int32_t radius, int32_t prev_dilation, int32_t projection,
+                            int32_t* const* row_ptrs, int32_t* const* col_idxs,
+                            const int64_t* capacities, int32_t* const* orders, hipStream_t stream);
 
 /*
  * Block-sparse cross-scale attention at scale k (the sparse update

@@ -6,6 +6,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <string>
 
 #include "geometry.h"
 #include "launch.h"
@@ -167,6 +168,35 @@ int check_select_limits(const GeoTable& T, int S, bool scoring) {
   if ((int64_t)NB * 8 > 64 * 1024) return fail(SPARVAR_ERR_UNSUPPORTED, "%d candidate blocks exceed the selection kernel's LDS", NB);
   if (scoring && T.eh[S - 1] * T.ew[S - 1] > 256)
     return fail(SPARVAR_ERR_UNSUPPORTED, "query tiles above 256 tokens are not supported by the scoring kernel");
+  return SPARVAR_OK;
+}
+
+// Row slots of a mapping step: the longest local row plus topk selected blocks,
+// each of which maps to one block (point projection) or to a cover box of at
+// most `cover` blocks. Validates the shared mapping arguments.
+struct MapSlots {
+  int32_t max_local, cover, per_row;
+  int64_t rows, need;  // rows, and the capacity they need (row slots, then one length per row)
+};
+
+int map_slots(const GeoTable& T, int32_t S, int32_t k, int32_t B, int32_t H, int32_t topk, int32_t radius,
+              int32_t dil, int32_t projection, MapSlots* m) {
+  if (S < 1 || k > T.L || S >= k) return fail(SPARVAR_ERR_INVALID, "need 1 <= S < k <= %d (S=%d, k=%d)", T.L, S, k);
+  if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
+  if (topk < 1 || topk > 1024) return fail(SPARVAR_ERR_INVALID, "topk %d outside [1, 1024]", topk);
+  if (radius < 0 || dil < 0) return fail(SPARVAR_ERR_INVALID, "radius and dilation must be >= 0");
+  if (projection != SPARVAR_PROJECT_POINT && projection != SPARVAR_PROJECT_COVER)
+    return fail(SPARVAR_ERR_INVALID, "projection %d is not SPARVAR_PROJECT_POINT or SPARVAR_PROJECT_COVER", projection);
+  m->max_local = local_max_len(T, k, radius, dil, nullptr);
+  m->cover = projection == SPARVAR_PROJECT_COVER ? max_cover_size(T, S, k) : 0;
+  const int64_t per_row = (int64_t)m->max_local + (int64_t)topk * (m->cover > 0 ? m->cover : 1);
+  m->rows = (int64_t)B * H * tiles_of(T, k);
+  m->need = m->rows * per_row + m->rows;
+  if (m->rows >= (int64_t(1) << 31) || m->need >= (int64_t(1) << 31))
+    return fail(SPARVAR_ERR_INVALID, "index lists too large for int32 offsets");
+  if (per_row * 2 * 4 * 4 > 64 * 1024)
+    return fail(SPARVAR_ERR_UNSUPPORTED, "rows of %lld candidates exceed the merge kernel's LDS", (long long)per_row);
+  m->per_row = (int32_t)per_row;
   return SPARVAR_OK;
 }
 
@@ -662,47 +692,34 @@ int sparvar_local_blocks(const sparvar_geometry_t* g, int32_t k, int32_t radius,
 
 int64_t sparvar_map_index_capacity(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t B,
                                    int32_t H, int32_t topk, int32_t radius,
-                                   int32_t prev_dilation) {
+                                   int32_t prev_dilation, int32_t projection) {
   GeoTable T;
   int st = build_table(g, &T);
   if (st) return st;
-  if (S < 1 || k > T.L || S >= k) return fail(SPARVAR_ERR_INVALID, "need 1 <= S < k <= %d (S=%d, k=%d)", T.L, S, k);
-  if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
-  if (topk < 1 || topk > 1024) return fail(SPARVAR_ERR_INVALID, "topk %d outside [1, 1024]", topk);
-  if (radius < 0 || prev_dilation < 0) return fail(SPARVAR_ERR_INVALID, "radius and dilation must be >= 0");
-  const int32_t mx = local_max_len(T, k, radius, prev_dilation, nullptr);
+  MapSlots m;
+  if ((st = map_slots(T, S, k, B, H, topk, radius, prev_dilation, projection, &m))) return st;
   ok();
-  const int64_t rows = (int64_t)B * H * tiles_of(T, k);
-  return rows * (int64_t)(mx + topk) + rows;  // row entries, then per-row counts
+  return m.need;
 }
 
 int sparvar_map_index(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t B, int32_t H,
                       int32_t topk, const int32_t* topk_idx, const int32_t* local_row_ptr,
                       const int32_t* local_col_idx, int32_t radius, int32_t prev_dilation,
-                      int32_t* row_ptr, int32_t* col_idx, int64_t capacity, int32_t* schedule,
-                      int32_t* status, hipStream_t stream) {
+                      int32_t projection, int32_t* row_ptr, int32_t* col_idx, int64_t capacity,
+                      int32_t* schedule, int32_t* status, hipStream_t stream) {
   GeoTable T;
   int st = build_table(g, &T);
   if (st) return st;
-  if (S < 1 || k > T.L || S >= k) return fail(SPARVAR_ERR_INVALID, "need 1 <= S < k <= %d (S=%d, k=%d)", T.L, S, k);
-  if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
-  if (topk < 1 || topk > 1024) return fail(SPARVAR_ERR_INVALID, "topk %d outside [1, 1024]", topk);
-  if (radius < 0 || prev_dilation < 0) return fail(SPARVAR_ERR_INVALID, "radius and dilation must be >= 0");
+  MapSlots m;
+  if ((st = map_slots(T, S, k, B, H, topk, radius, prev_dilation, projection, &m))) return st;
   if (!topk_idx || !row_ptr || !col_idx || (!local_row_ptr) != (!local_col_idx))
     return fail(SPARVAR_ERR_INVALID, "a required pointer is NULL");
-  const int32_t mx = local_max_len(T, k, radius, prev_dilation, nullptr);
-  const int64_t rows = (int64_t)B * H * tiles_of(T, k);
-  const int64_t bound = rows * (int64_t)(mx + topk);
-  const int64_t need = bound + rows;
-  if (rows >= (int64_t(1) << 31) || need >= (int64_t(1) << 31))
-    return fail(SPARVAR_ERR_INVALID, "index lists too large for int32 offsets");
-  if (capacity < need)
-    return fail(SPARVAR_ERR_CAPACITY, "capacity %lld < bound %lld", (long long)capacity, (long long)need);
-  if ((int64_t)(mx + topk) * 2 * 4 * 4 > 64 * 1024)
-    return fail(SPARVAR_ERR_UNSUPPORTED, "rows of %d candidates exceed the merge kernel's LDS", mx + topk);
+  if (capacity < m.need)
+    return fail(SPARVAR_ERR_CAPACITY, "capacity %lld < bound %lld", (long long)capacity, (long long)m.need);
   MapStepArgs sa;
   sa.k = k;
-  sa.max_local = mx;
+  sa.max_local = m.max_local;
+  sa.cover = m.cover;
   sa.local_row_ptr = local_row_ptr;
   sa.local_col_idx = local_col_idx;
   sa.row_ptr = row_ptr;
@@ -714,38 +731,30 @@ int sparvar_map_index(const sparvar_geometry_t* g, int32_t S, int32_t k, int32_t
 
 int sparvar_map_index_steps(const sparvar_geometry_t* g, int32_t S, int32_t n_steps, const int32_t* ks, int32_t B,
                             int32_t H, int32_t topk, const int32_t* topk_idx, int32_t radius, int32_t prev_dilation,
-                            int32_t* const* row_ptrs, int32_t* const* col_idxs, const int64_t* capacities,
-                            int32_t* const* orders, hipStream_t stream) {
+                            int32_t projection, int32_t* const* row_ptrs, int32_t* const* col_idxs,
+                            const int64_t* capacities, int32_t* const* orders, hipStream_t stream) {
   GeoTable T;
   int st = build_table(g, &T);
   if (st) return st;
   if (n_steps < 1 || n_steps > kMaxMapSteps)
     return fail(SPARVAR_ERR_INVALID, "n_steps %d outside [1, %d]", n_steps, kMaxMapSteps);
   if (!ks || !row_ptrs || !col_idxs || !capacities) return fail(SPARVAR_ERR_INVALID, "a step array is NULL");
-  if (B < 1 || H < 1) return fail(SPARVAR_ERR_INVALID, "B and H must be >= 1");
-  if (topk < 1 || topk > 1024) return fail(SPARVAR_ERR_INVALID, "topk %d outside [1, 1024]", topk);
-  if (radius < 0 || prev_dilation < 0) return fail(SPARVAR_ERR_INVALID, "radius and dilation must be >= 0");
   if (!topk_idx) return fail(SPARVAR_ERR_INVALID, "topk_idx is NULL");
   MapStepArgs sa[kMaxMapSteps];
   int64_t blocks = 0;
   for (int i = 0; i < n_steps; ++i) {
     const int32_t k = ks[i];
-    if (S < 1 || k > T.L || S >= k)
-      return fail(SPARVAR_ERR_INVALID, "step %d: need 1 <= S < k <= %d (S=%d, k=%d)", i, T.L, S, k);
+    MapSlots m;
+    if ((st = map_slots(T, S, k, B, H, topk, radius, prev_dilation, projection, &m)))
+      return fail(st, "step %d: %s", i, std::string(g_last_error).c_str());
     if (!row_ptrs[i] || !col_idxs[i]) return fail(SPARVAR_ERR_INVALID, "step %d: row_ptr/col_idx is NULL", i);
-    const int32_t mx = local_max_len(T, k, radius, prev_dilation, nullptr);
-    const int64_t rows = (int64_t)B * H * tiles_of(T, k);
-    const int64_t need = rows * (int64_t)(mx + topk) + rows;
-    if (rows >= (int64_t(1) << 31) || need >= (int64_t(1) << 31))
-      return fail(SPARVAR_ERR_INVALID, "step %d: index lists too large for int32 offsets", i);
-    if (capacities[i] < need)
+    if (capacities[i] < m.need)
       return fail(SPARVAR_ERR_CAPACITY, "step %d: capacity %lld < bound %lld", i, (long long)capacities[i],
-                  (long long)need);
-    if ((int64_t)(mx + topk) * 2 * 4 * 4 > 64 * 1024)
-      return fail(SPARVAR_ERR_UNSUPPORTED, "step %d: rows of %d candidates exceed the merge kernel's LDS", i, mx + topk);
-    blocks += (rows + 3) / 4;
+                  (long long)m.need);
+    blocks += (m.rows + 3) / 4;
     sa[i].k = k;
-    sa[i].max_local = mx;
+    sa[i].max_local = m.max_local;
+    sa[i].cover = m.cover;
     sa[i].local_row_ptr = nullptr;
     sa[i].local_col_idx = nullptr;
     sa[i].row_ptr = row_ptrs[i];

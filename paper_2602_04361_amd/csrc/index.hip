@@ -68,6 +68,7 @@ struct MapStep {
   int32_t* counts;  // [rows] row lengths
   int32_t* status;  // nullable: receives kStatusCut when a supplied local row is cut
   int32_t k, G_k, rows, max_cand, block0;
+  int32_t cover;  // 0: point projection; else the largest cover box (candidates per selected block)
 };
 
 struct MapIO {
@@ -123,14 +124,16 @@ __global__ __launch_bounds__(kMapWaves * 64) void map_rows_kernel(MapIO io) {
       n_loc = local_row_len(lr);
     }
     if (n_loc < 0) n_loc = 0;
-    if (n_loc > ms.max_cand - io.topk) {
+    const int32_t loc_cap = ms.max_cand - io.topk * (ms.cover > 0 ? ms.cover : 1);
+    if (n_loc > loc_cap) {
       // a supplied local row longer than the (radius, dilation) bound: cut to
       // the bound, and reported through the caller's status word
-      n_loc = ms.max_cand - io.topk;
+      n_loc = loc_cap;
       if (ms.status && lane == 0) *ms.status = kStatusCut;
     }
   }
-  const int32_t n = active ? n_loc + io.topk : 0;
+  const int32_t per_sel = ms.cover > 0 ? ms.cover : 1;
+  const int32_t n = active ? n_loc + io.topk * per_sel : 0;
   const int32_t* sel = io.topk_idx + ((int64_t)bh * io.G_S + gs) * io.topk;
   const int32_t nb_S = G.NB[io.S], nb_k = G.NB[k];
   for (int32_t i = lane; i < n; i += 64) {
@@ -138,9 +141,19 @@ __global__ __launch_bounds__(kMapWaves * 64) void map_rows_kernel(MapIO io) {
     if (i < n_loc) {
       v = ms.local_row_ptr ? ms.local_col[lp + i] : local_row_entry(G, k, lr, i);
       if (v < 0 || v >= nb_k) v = kInvalid;
-    } else {
+    } else if (ms.cover == 0) {
       const int32_t s = sel[i - n_loc];
       v = (s >= 0 && s < nb_S) ? map_block(G, s, io.S, k) : kInvalid;
+    } else {
+      // covering projection: slot j of selected block i / cover is the j-th tile
+      // of its cover box, if the box has that many
+      const int32_t q = (i - n_loc) / ms.cover, j = (i - n_loc) - q * ms.cover;
+      const int32_t s = sel[q];
+      v = kInvalid;
+      if (s >= 0 && s < nb_S) {
+        const CoverBox b = map_block_cover(G, s, io.S, k);
+        if (j < cover_size(b)) v = cover_entry(b, j);
+      }
     }
     cand[i] = v;
   }
@@ -289,7 +302,8 @@ hipError_t launch_map_order(const GeoTable& G, int32_t BH, int32_t topk, int n_s
     const SparseForm f = sparse_form(G, k, BH, num_cu, group_waves);
     const int32_t rows = BH * tiles_of(G, k);
     o.order = orders ? orders[i] : nullptr;
-    o.counts = steps[i].col_idx + (int64_t)rows * (steps[i].max_local + topk);  // the row lengths after the slots
+    const int32_t per_sel = steps[i].cover > 0 ? steps[i].cover : 1;
+    o.counts = steps[i].col_idx + (int64_t)rows * (steps[i].max_local + topk * per_sel);  // row lengths after the slots
     o.n_items = o.order ? f.n_items : 0;
     o.per = (o.n_items + 7) / 8;
     o.G_k = tiles_of(G, k);
@@ -330,7 +344,8 @@ hipError_t launch_map_index(const GeoTable& G, int S, int32_t BH, int32_t topk, 
     m.k = a.k;
     m.G_k = tiles_of(G, a.k);
     m.rows = BH * m.G_k;
-    m.max_cand = a.max_local + topk;
+    m.cover = a.cover;
+    m.max_cand = a.max_local + topk * (a.cover > 0 ? a.cover : 1);
     m.counts = a.col_idx + (int64_t)m.rows * m.max_cand;  // past the last row slot
     m.status = a.status;
     m.block0 = blocks;

@@ -155,12 +155,13 @@ hipError_t launch_topk(const float* scores, int32_t rows, int32_t nb, int32_t to
 hipError_t launch_local_blocks(const GeoTable& G, int k, int32_t radius, int32_t dil, int32_t* row_ptr,
                                int32_t* col_idx, hipStream_t stream);
 // One target scale of a map launch. max_local bounds its local rows; row slots
-// are max_local + topk wide, and the row lengths follow the last slot.
+// are max_local + topk * max(cover, 1) wide, and the row lengths follow the last slot.
 struct MapStepArgs {
   int32_t k, max_local;
   const int32_t *local_row_ptr, *local_col_idx;  // both NULL: generated
   int32_t *row_ptr, *col_idx;
   int32_t* status;  // nullable: set to SPARVAR_ERR_CAPACITY when a supplied local row is cut to max_local
+  int32_t cover = 0;  // 0: point projection; else covering, with boxes of at most `cover` tiles
 };
 constexpr int kMaxMapSteps = 8;
 // Rows of every listed step in one launch; the schedule (single step only) is

@@ -25,7 +25,7 @@ from . import sparvar as sv
 class SparsePath:
     def __init__(self, geom: sv.Geometry, S, steps, B, H, d, topk, radius, prev_dilation=0,
                  dtype=torch.bfloat16, device="cuda", use_schedule=False, softmax_scale=None, local_lists=False,
-                 fused_decision=True):
+                 fused_decision=True, projection="point"):
         self.g = geom
         self.S, self.steps = int(S), [int(k) for k in steps]
         self.B, self.H, self.d = B, H, d
@@ -35,6 +35,8 @@ class SparsePath:
         # pass them to the mapping; otherwise the mapping generates them itself.
         self.local_lists = local_lists
         self.fused_decision = fused_decision
+        # projection of the mapped blocks: "point" (tile origin) or "cover" (every tile of the upsampled span)
+        self.projection = sv.PROJECTIONS[projection]
         self.scale = float(torch.tensor(1.0 / math.sqrt(d), dtype=torch.float32)) if softmax_scale is None \
             else float(softmax_scale)
         info = {l: geom.scale_info(l) for l in range(1, len(geom.h) + 1)}
@@ -52,7 +54,7 @@ class SparsePath:
             G_k = ik["tiles_h"] * ik["tiles_w"]
             cap_l = sv.sparvar_local_blocks_capacity(geom, k, radius, prev_dilation)
             self.local[k] = (torch.empty(G_k + 1, **i32), torch.empty(max(cap_l, 1), **i32))
-            cap = sv.sparvar_map_index_capacity(geom, S, k, B, H, topk, radius, prev_dilation)
+            cap = sv.sparvar_map_index_capacity(geom, S, k, B, H, topk, radius, prev_dilation, self.projection)
             rows = B * H * G_k
             self.csr[k] = (torch.empty(rows + 1, **i32), torch.empty(cap, **i32),
                            torch.empty(rows, **i32) if use_schedule else None)
@@ -87,7 +89,7 @@ class SparsePath:
         rp_l, ci_l = self.local[k] if self.local_lists else (None, None)
         rp, ci, sch = self.csr[k]
         sv.sparvar_map_index(self.g, self.S, k, self.B, self.H, self.topk, self.topk_idx, rp_l, ci_l, self.radius,
-                             rp, ci, schedule=sch, prev_dilation=self.dil)
+                             rp, ci, schedule=sch, prev_dilation=self.dil, projection=self.projection)
 
     def map_all(self, orders=False):
         """The rows of every sparse step in one launch (generated local rows); with orders, also each step's
@@ -98,7 +100,7 @@ class SparsePath:
                            for k in self.steps}
         sv.sparvar_map_index_steps(self.g, self.S, self.steps, self.B, self.H, self.topk, self.topk_idx, self.radius,
                                    [self.csr[k][0] for k in self.steps], [self.csr[k][1] for k in self.steps],
-                                   prev_dilation=self.dil,
+                                   prev_dilation=self.dil, projection=self.projection,
                                    orders=[self.orders[k] for k in self.steps] if orders else None)
 
     def attn_step(self, k, Q_all, K_all, V_all, lse=None, use_schedule=True, use_order=False):

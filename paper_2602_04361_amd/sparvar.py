@@ -52,6 +52,10 @@ LAUNCH_OPTIONS = ["SWIZZLE", "DENSE_WAVES", "DENSE_CHUNK", "DENSE_STAGES", "SPAR
                   "SPARSE_STAGES", "SPARSE_GROUP_WAVES", "SPARSE_GROUP_CHUNK", "SPARSE_GROUP_STAGES", "CSLA_CHUNK",
                   "CSLA_STAGES", "CS4A_CHUNK", "DECISION_FUSED"]
 OPT_DEFAULT = -(1 << 31)
+# sparvar_projection_t
+PROJECT_POINT, PROJECT_COVER = 0, 1
+PROJECTIONS = {"point": PROJECT_POINT, "cover": PROJECT_COVER, PROJECT_POINT: PROJECT_POINT,
+               PROJECT_COVER: PROJECT_COVER}
 
 
 class SparvarError(RuntimeError):
@@ -101,8 +105,8 @@ def load_library(path: str = LIB_PATH):
                                                     f32, vp, vp]),
         "sparvar_cs4a_select_tokens": (ctypes.c_int, [vp, i32, i32, i32, vp, vp]),
         "sparvar_cs4a_row_stride": (i32, [G, i32]),
-        "sparvar_map_index_steps": (ctypes.c_int, [G, i32, i32, vp, i32, i32, i32, vp, i32, i32, vp, vp, vp, vp,
-                                                   vp]),
+        "sparvar_map_index_steps": (ctypes.c_int, [G, i32, i32, vp, i32, i32, i32, vp, i32, i32, i32, vp, vp, vp,
+                                                   vp, vp]),
         "sparvar_kv_compact": (ctypes.c_int, [G, i32, vp, i32, i32, i32, ctypes.c_int, vp, vp, i64, vp, vp, i64, vp]),
         "sparvar_csla_row_stride": (i32, [G, i32, i32]),
         "sparvar_csla_block_rows": (ctypes.c_int, [G, i32, vp, i32, vp, i32, vp]),
@@ -113,9 +117,9 @@ def load_library(path: str = LIB_PATH):
                                                  vp, f32, vp, i32, i32, vp, i32, vp]),
         "sparvar_local_blocks_capacity": (i64, [G, i32, i32, i32]),
         "sparvar_local_blocks": (ctypes.c_int, [G, i32, i32, i32, vp, vp, i64, vp]),
-        "sparvar_map_index_capacity": (i64, [G, i32, i32, i32, i32, i32, i32, i32]),
-        "sparvar_map_index": (ctypes.c_int, [G, i32, i32, i32, i32, i32, vp, vp, vp, i32, i32, vp, vp, i64, vp, vp,
-                                             vp]),
+        "sparvar_map_index_capacity": (i64, [G, i32, i32, i32, i32, i32, i32, i32, i32]),
+        "sparvar_map_index": (ctypes.c_int, [G, i32, i32, i32, i32, i32, vp, vp, vp, i32, i32, i32, vp, vp, i64, vp,
+                                             vp, vp]),
         "sparvar_block_sparse_attn_fwd": (ctypes.c_int, [G, i32, i32, i32, i32, ctypes.c_int, vp, i64, vp, vp, i64,
                                                          vp, vp, f32, vp, vp, vp, vp]),
         "sparvar_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -385,26 +389,28 @@ def sparvar_local_blocks(geom, k, radius, row_ptr, col_idx, prev_dilation=0, str
     return row_ptr, col_idx
 
 
-def sparvar_map_index_capacity(geom, S, k, B, H, topk, radius, prev_dilation=0):
-    n = load_library().sparvar_map_index_capacity(geom.ref, S, k, B, H, topk, radius, prev_dilation)
+def sparvar_map_index_capacity(geom, S, k, B, H, topk, radius, prev_dilation=0, projection=PROJECT_POINT):
+    n = load_library().sparvar_map_index_capacity(geom.ref, S, k, B, H, topk, radius, prev_dilation,
+                                                  PROJECTIONS[projection])
     if n < 0:
         _check(int(n))
     return int(n)
 
 
 def sparvar_map_index(geom, S, k, B, H, topk, topk_idx, local_row_ptr, local_col_idx, radius, row_ptr, col_idx,
-                      schedule=None, prev_dilation=0, status=None, stream=None):
+                      schedule=None, prev_dilation=0, status=None, projection=PROJECT_POINT, stream=None):
     """Mapped + local blocks -> CSR; local_row_ptr/local_col_idx may both be None. status (optional one-element
     int32 device tensor, cleared by the caller) receives ERR_CAPACITY if a supplied local row was cut."""
     _check(load_library().sparvar_map_index(geom.ref, S, k, B, H, topk, _ptr(topk_idx), _ptr(local_row_ptr),
-                                            _ptr(local_col_idx), radius, prev_dilation, _ptr(row_ptr),
+                                            _ptr(local_col_idx), radius, prev_dilation, PROJECTIONS[projection],
+                                            _ptr(row_ptr),
                                             _ptr(col_idx), col_idx.numel(), _ptr(schedule), _ptr(status),
                                             _stream(stream)))
     return row_ptr, col_idx, schedule
 
 
 def sparvar_map_index_steps(geom, S, ks, B, H, topk, topk_idx, radius, row_ptrs, col_idxs, prev_dilation=0,
-                            orders=None, stream=None):
+                            orders=None, projection=PROJECT_POINT, stream=None):
     """The rows of several target scales in one launch (local rows generated); with orders (one int32 tensor of
     B*H*G_k entries, or None, per step) also the attention launch order of each step."""
     n = len(ks)
@@ -421,7 +427,8 @@ def sparvar_map_index_steps(geom, S, ks, B, H, topk, topk_idx, radius, row_ptrs,
             raise SparvarError(ERR_INVALID, "one order (or None) per step is required")
         ord_arr = (ctypes.c_void_p * max(n, 1))(*[(t.data_ptr() if t is not None else None) for t in orders])
     _check(load_library().sparvar_map_index_steps(geom.ref, S, n, ctypes.cast(k_arr, vp), B, H, topk,
-                                                  _ptr(topk_idx), radius, prev_dilation, ctypes.cast(rp_arr, vp),
+                                                  _ptr(topk_idx), radius, prev_dilation, PROJECTIONS[projection],
+                                                  ctypes.cast(rp_arr, vp),
                                                   ctypes.cast(ci_arr, vp), ctypes.cast(cap_arr, vp),
                                                   ctypes.cast(ord_arr, vp) if ord_arr is not None else None,
                                                   _stream(stream)))

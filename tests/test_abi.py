@@ -65,19 +65,36 @@ def test_map_capacity_bound():
     assert sv.sparvar_map_index_capacity(g, 10, 13, 2, 16, 8, 1) == rows_n * (max(map(len, rows)) + 8) + rows_n
 
 
+def test_map_capacity_bound_cover():
+    # covering projection: each selected block takes as many slots as the largest
+    # cover box of a block of scales 1..S (from the oracle's cover map)
+    from oracle import map_block_cover
+    for sides, b, S, k, topk in [(INF, 8, 10, 13, 8), (INF, 8, 10, 11, 8), (INF, 16, 10, 12, 4),
+                                 (INF + [80, 96, 128], 8, 13, 16, 16), ([1, 2, 3, 5, 7, 10, 13], 3, 4, 7, 3)]:
+        og = OGeom(sides, sides, b, 4)
+        g = sv.Geometry(sides, sides, b, 4)
+        mx_cover = max(len(map_block_cover(og, v, S, k)) for v in range(og.nb_le(S)))
+        mx_local = max(map(len, o_local_blocks(og, k, 1)))
+        rows_n = 2 * 3 * og.tiles(k)
+        want = rows_n * (mx_local + topk * mx_cover) + rows_n
+        assert sv.sparvar_map_index_capacity(g, S, k, 2, 3, topk, 1, projection="cover") == want
+    assert max(len(map_block_cover(OGeom(INF, INF, 8, 4), v, 10, 13)) for v in range(47)) == 9
+
+
 @pytest.mark.parametrize("args,status", [
     (dict(S=13, k=13), sv.ERR_INVALID),
     (dict(S=0, k=13), sv.ERR_INVALID),
     (dict(topk=0), sv.ERR_INVALID),
     (dict(topk=2000), sv.ERR_INVALID),
     (dict(radius=-1), sv.ERR_INVALID),
+    (dict(projection=2), sv.ERR_INVALID),
 ])
 def test_map_capacity_rejects(args, status):
     g = sv.Geometry(INF, INF, 8, 4)
     a = dict(S=10, k=13, B=2, H=16, topk=8, radius=1)
     a.update(args)
     n = sv.load_library().sparvar_map_index_capacity(g.ref, a["S"], a["k"], a["B"], a["H"], a["topk"],
-                                                     a["radius"], 0)
+                                                     a["radius"], 0, a.get("projection", 0))
     assert n == status
     assert sv.load_library().sparvar_last_error()
 
@@ -127,7 +144,7 @@ def test_attention_validation_before_launch():
     assert lib.sparvar_select_blocks(g.ref, 10, 1, 1, 128, sv.BF16, fake, 1024 * 128, fake, 2521 * 128, fake, 0.1,
                                      None, None, 8, fake, None) == sv.ERR_INVALID
     assert lib.sparvar_local_blocks(g.ref, 13, 1, 0, fake, fake, 10, None) == sv.ERR_CAPACITY
-    assert lib.sparvar_map_index(g.ref, 10, 13, 1, 1, 8, fake, fake, fake, 1, 0, fake, fake, 10, None, None,
+    assert lib.sparvar_map_index(g.ref, 10, 13, 1, 1, 8, fake, fake, fake, 1, 0, 0, fake, fake, 10, None, None,
                                  None) == sv.ERR_CAPACITY
     assert b"capacity" in lib.sparvar_last_error()
 
@@ -201,7 +218,7 @@ def test_map_steps_validation_before_launch():
         k_arr = (ctypes.c_int32 * 3)(*ks)
         p_arr = (ctypes.c_void_p * 3)(rp, fake, fake)
         c_arr = (ctypes.c_int64 * 3)(*caps)
-        return lib.sparvar_map_index_steps(g.ref, S, n, ctypes.cast(k_arr, vp), 2, 16, topk, vp(fake), 1, 0,
+        return lib.sparvar_map_index_steps(g.ref, S, n, ctypes.cast(k_arr, vp), 2, 16, topk, vp(fake), 1, 0, 0,
                                            ctypes.cast(p_arr, vp), ctypes.cast(p_arr, vp), ctypes.cast(c_arr, vp), None,
                                            None)
     assert call(0, (11, 12, 13), cap) == sv.ERR_INVALID            # no step

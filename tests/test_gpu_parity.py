@@ -20,15 +20,15 @@ LSE_TOL = {"bf16": 2e-4, "f32": 1e-5}
 
 
 def run_case(h, w, b, ns, S, steps, B, H, d, F, topk, r, dtype, seed=0, dil=0, heads=None, tiles_per_step=None,
-             check_schedule=True):
+             check_schedule=True, projection="point"):
     note(f"[case] h={h} w={w} b={b} ns={ns} S={S} steps={steps} B={B} H={H} d={d} topk={topk} r={r} "
-         f"dil={dil} {dtype} seed={seed}")
+         f"dil={dil} {dtype} seed={seed} projection={projection}")
     q, k, v = make_case(h, w, B, H, d, F, ns, seed, dtype)
     Qd, Kd, Vd = to_dev(q, dtype), to_dev(k, dtype), to_dev(v, dtype)
     g = sv.Geometry(h, w, b, ns)
     og = oracle_geometry(h, w, b, ns)
     path = SparsePath(g, S, steps, B, H, d, topk, r, dil, dtype=torch_dtype(dtype), use_schedule=True,
-                      local_lists=True)
+                      local_lists=True, projection=projection)
     path.build_local()
     path.decision(Qd, Kd, Vd)
     lse_k = {}
@@ -70,7 +70,7 @@ def run_case(h, w, b, ns, S, steps, B, H, d, F, topk, r, dtype, seed=0, dil=0, h
         loc = O.local_blocks(og, kk, r, dil)
         assert csr_rows(*path.local[kk]) == loc, f"local rows step {kk}"
         # merged rows: bit-exact
-        rows = O.build_rows(og, S, kk, tk, loc)
+        rows = O.build_rows(og, S, kk, tk, loc, projection=projection)
         rp, ci, sch = path.csr[kk]
         got = csr_rows(rp, ci, padded=True)
         assert got == [r_ for per in rows for r_ in per], f"CSR rows step {kk}"
@@ -183,6 +183,29 @@ def test_sparsity_sweep_settings_full_size(b, topk, r):
     # 1 and 2. Index lists bit-exact on all heads; attention sampled on two heads.
     run_case(INF_SIDES, INF_SIDES, b, 4, 10, [11, 12, 13], 2, 16, 128, 32, topk, r, "bf16", seed=40 + topk + r,
              heads=[3, 26], tiles_per_step=6)
+
+
+def test_cover_projection_infinity_full_size():
+    # covering projection of the mapped blocks on the Infinity layer (B=2, H=16,
+    # d=128, S=32x32, top-8, r=1): every index list bit-exact on all heads,
+    # attention sampled on three heads
+    run_case(INF_SIDES, INF_SIDES, 8, 4, 10, [11, 12, 13], 2, 16, 128, 32, 8, 1, "bf16", seed=90,
+             heads=[0, 17, 31], tiles_per_step=12, projection="cover")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_cover_projection_odd_nonsquare(dtype):
+    # non-square scales with odd sides and a non-integer ratio between aligned scales
+    h = [1, 2, 3, 5, 8, 11]
+    w = [1, 3, 4, 7, 9, 14]
+    run_case(h, w, 4, 1, 3, [4, 5, 6], 1, 2, 64, 8, 3, 1, dtype, seed=91, dil=1, projection="cover")
+
+
+def test_cover_projection_2048_schedule_sampled():
+    # the 2048x2048-shaped schedule, decision at 64x64, top-16, covering projection
+    sides = INF_SIDES + [80, 96, 128]
+    run_case(sides, sides, 8, 4, 13, [14, 15, 16], 1, 16, 128, 32, 16, 1, "bf16", seed=92, heads=[0, 9],
+             tiles_per_step=8, projection="cover")
 
 
 # ---------------------------------------------------------------- dense kernel edge cases

@@ -1,10 +1,11 @@
 """GPU parity on randomly drawn small schedules: non-square and odd scale sides,
 block edges 2-16, sink scales, top-k, radius and dilation, head dim 64 or 128,
-bf16 and fp32. Every case runs the whole layer (dense decision scale with pooled
-scores and top-k, local lists, mapping to CSR rows with a launch order, and the
-block-sparse steps) through the C ABI and checks it against the fp64 oracle to
-the same bar as the hand-picked cases: rows bit-exact, attention within
-tolerance on every query tile."""
+bf16 and fp32, point and covering projection of the mapped blocks. Every case
+runs the whole layer (dense decision scale with pooled scores and top-k, local
+lists, mapping to CSR rows with a launch order, and the block-sparse steps)
+through the C ABI and checks it against the fp64 oracle to the same bar as the
+hand-picked cases: rows bit-exact, attention within tolerance on every query
+tile."""
 import numpy as np
 import pytest
 
@@ -31,11 +32,11 @@ def draw_schedule(seed):
     steps = list(range(S + 1, min(L, S + 3) + 1))
     return dict(h=h, w=w, b=b, ns=ns, S=S, steps=steps, B=1, H=2, d=int(rng.choice([64, 128])),
                 F=4, topk=int(rng.integers(1, 13)), r=int(rng.integers(0, 3)), dil=int(rng.integers(0, 2)),
-                dtype=["bf16", "f32"][seed % 2], seed=seed)
+                dtype=["bf16", "f32"][seed % 2], seed=seed, projection=["point", "cover"][(seed // 2) % 2])
 
 
 @pytest.mark.parametrize("seed", range(32))
 def test_random_schedule(seed):
     c = draw_schedule(seed)
     run_case(c["h"], c["w"], c["b"], c["ns"], c["S"], c["steps"], c["B"], c["H"], c["d"], c["F"], c["topk"],
-             c["r"], c["dtype"], seed=c["seed"], dil=c["dil"])
+             c["r"], c["dtype"], seed=c["seed"], dil=c["dil"], projection=c["projection"])
