@@ -363,6 +363,28 @@ int sparvar_map_index_steps(const sparvar_geometry_t* g, int32_t S, int32_t n_st
                             const int64_t* capacities, int32_t* const* orders, hipStream_t stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * call and results as sparvar_map_index_steps, but the per-row lengths that
+ * call keeps after the row slots of each col_idxs[i] (and that its launch
+ * orders are ranked from) live in a fixed array of SPARVAR_NOALLOC_MAX_ROWS
+ * int32 inside the library, one per device, held until the process ends. So
+ * capacities[i] only need the row slots: sparvar_map_index_capacity(...) minus
+ * B*H*G_k of ks[i]. The call allocates nothing; the first call on a device
+ * looks up that device's array. The array is shared by every call on a
+ * device: calls that overlap on one device race (serialise them, e.g. on one
+ * stream). Fails with SPARVAR_ERR_CAPACITY when the steps' rows (B*H*G_k
+ * summed over the steps) exceed SPARVAR_NOALLOC_MAX_ROWS.
+ */
+#define SPARVAR_NOALLOC_MAX_ROWS (1 << 20) /* 4 MiB of row lengths per device */
+int sparvar_map_index_steps_noalloc(const sparvar_geometry_t* g, int32_t S, int32_t n_steps,
+                                    const int32_t* ks, int32_t B, int32_t H, int32_t topk,
+                                    const int32_t* topk_idx, int32_t radius, int32_t prev_dilation,
+                                    int32_t projection, int32_t* const* row_ptrs,
+                                    int32_t* const* col_idxs, const int64_t* capacities,
+                                    int32_t* const* orders, hipStream_t stream);
+
+/*
  * Block-sparse cross-scale attention at scale k (the sparse update
  * Delta O of Sec. 3.2 and the block-masked attention of Sec. 3.3, Eq. (3)):
  * every query of query tile g of (b,h) attends, with one softmax, to exactly

@@ -200,6 +200,66 @@ int map_slots(const GeoTable& T, int32_t S, int32_t k, int32_t B, int32_t H, int
   return SPARVAR_OK;
 }
 
+// Mapping of several steps in one launch (sparvar_map_index_steps). With
+// noalloc, the per-row lengths the map kernel writes (and the order kernel
+// reads) go to the library's fixed per-device scratch instead of the tail of
+// each col_idxs[i], so the capacities only need the row slots.
+int map_steps(const sparvar_geometry_t* g, int32_t S, int32_t n_steps, const int32_t* ks, int32_t B, int32_t H,
+              int32_t topk, const int32_t* topk_idx, int32_t radius, int32_t prev_dilation, int32_t projection,
+              int32_t* const* row_ptrs, int32_t* const* col_idxs, const int64_t* capacities, int32_t* const* orders,
+              bool noalloc, hipStream_t stream) {
+  GeoTable T;
+  int st = build_table(g, &T);
+  if (st) return st;
+  if (n_steps < 1 || n_steps > kMaxMapSteps)
+    return fail(SPARVAR_ERR_INVALID, "n_steps %d outside [1, %d]", n_steps, kMaxMapSteps);
+  if (!ks || !row_ptrs || !col_idxs || !capacities) return fail(SPARVAR_ERR_INVALID, "a step array is NULL");
+  if (!topk_idx) return fail(SPARVAR_ERR_INVALID, "topk_idx is NULL");
+  MapStepArgs sa[kMaxMapSteps];
+  int64_t blocks = 0, all_rows = 0;
+  for (int i = 0; i < n_steps; ++i) {
+    const int32_t k = ks[i];
+    MapSlots m;
+    if ((st = map_slots(T, S, k, B, H, topk, radius, prev_dilation, projection, &m)))
+      return fail(st, "step %d: %s", i, std::string(g_last_error).c_str());
+    if (!row_ptrs[i] || !col_idxs[i]) return fail(SPARVAR_ERR_INVALID, "step %d: row_ptr/col_idx is NULL", i);
+    const int64_t need = noalloc ? m.need - m.rows : m.need;
+    if (capacities[i] < need)
+      return fail(SPARVAR_ERR_CAPACITY, "step %d: capacity %lld < bound %lld", i, (long long)capacities[i],
+                  (long long)need);
+    blocks += (m.rows + 3) / 4;
+    sa[i].k = k;
+    sa[i].max_local = m.max_local;
+    sa[i].cover = m.cover;
+    sa[i].local_row_ptr = nullptr;
+    sa[i].local_col_idx = nullptr;
+    sa[i].row_ptr = row_ptrs[i];
+    sa[i].col_idx = col_idxs[i];
+    sa[i].status = nullptr;
+    sa[i].counts = nullptr;
+    all_rows += m.rows;
+  }
+  if (blocks >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "too many rows for one launch");
+  if (noalloc) {
+    if (all_rows > kNoAllocMaxRows)
+      return fail(SPARVAR_ERR_CAPACITY, "%lld rows exceed the %d row lengths of the fixed scratch",
+                  (long long)all_rows, kNoAllocMaxRows);
+    int32_t* lengths = nullptr;
+    if ((st = hip_status(noalloc_row_lengths(&lengths), "fixed scratch lookup"))) return st;
+    int64_t off = 0;
+    for (int i = 0; i < n_steps; ++i) {
+      sa[i].counts = lengths + off;
+      off += (int64_t)B * H * tiles_of(T, sa[i].k);
+    }
+  }
+  st = hip_status(launch_map_index(T, S, B * H, topk, topk_idx, radius, prev_dilation, n_steps, sa, nullptr, stream),
+                  "map index launch");
+  if (st || !orders) return st;
+  return hip_status(launch_map_order(T, B * H, topk, n_steps, sa, orders, device_cus(),
+                                     opt(SPARVAR_OPT_SPARSE_GROUP_WAVES), stream),
+                    "launch order launch");
+}
+
 }  // namespace
 
 extern "C" {
@@ -733,41 +793,17 @@ int sparvar_map_index_steps(const sparvar_geometry_t* g, int32_t S, int32_t n_st
                             int32_t H, int32_t topk, const int32_t* topk_idx, int32_t radius, int32_t prev_dilation,
                             int32_t projection, int32_t* const* row_ptrs, int32_t* const* col_idxs,
                             const int64_t* capacities, int32_t* const* orders, hipStream_t stream) {
-  GeoTable T;
-  int st = build_table(g, &T);
-  if (st) return st;
-  if (n_steps < 1 || n_steps > kMaxMapSteps)
-    return fail(SPARVAR_ERR_INVALID, "n_steps %d outside [1, %d]", n_steps, kMaxMapSteps);
-  if (!ks || !row_ptrs || !col_idxs || !capacities) return fail(SPARVAR_ERR_INVALID, "a step array is NULL");
-  if (!topk_idx) return fail(SPARVAR_ERR_INVALID, "topk_idx is NULL");
-  MapStepArgs sa[kMaxMapSteps];
-  int64_t blocks = 0;
-  for (int i = 0; i < n_steps; ++i) {
-    const int32_t k = ks[i];
-    MapSlots m;
-    if ((st = map_slots(T, S, k, B, H, topk, radius, prev_dilation, projection, &m)))
-      return fail(st, "step %d: %s", i, std::string(g_last_error).c_str());
-    if (!row_ptrs[i] || !col_idxs[i]) return fail(SPARVAR_ERR_INVALID, "step %d: row_ptr/col_idx is NULL", i);
-    if (capacities[i] < m.need)
-      return fail(SPARVAR_ERR_CAPACITY, "step %d: capacity %lld < bound %lld", i, (long long)capacities[i],
-                  (long long)m.need);
-    blocks += (m.rows + 3) / 4;
-    sa[i].k = k;
-    sa[i].max_local = m.max_local;
-    sa[i].cover = m.cover;
-    sa[i].local_row_ptr = nullptr;
-    sa[i].local_col_idx = nullptr;
-    sa[i].row_ptr = row_ptrs[i];
-    sa[i].col_idx = col_idxs[i];
-    sa[i].status = nullptr;
-  }
-  if (blocks >= (int64_t(1) << 31)) return fail(SPARVAR_ERR_INVALID, "too many rows for one launch");
-  st = hip_status(launch_map_index(T, S, B * H, topk, topk_idx, radius, prev_dilation, n_steps, sa, nullptr, stream),
-                  "map index launch");
-  if (st || !orders) return st;
-  return hip_status(launch_map_order(T, B * H, topk, n_steps, sa, orders, device_cus(),
-                                     opt(SPARVAR_OPT_SPARSE_GROUP_WAVES), stream),
-                    "launch order launch");
+  return map_steps(g, S, n_steps, ks, B, H, topk, topk_idx, radius, prev_dilation, projection, row_ptrs, col_idxs,
+                   capacities, orders, false, stream);
+}
+
+int sparvar_map_index_steps_noalloc(const sparvar_geometry_t* g, int32_t S, int32_t n_steps, const int32_t* ks,
+                                    int32_t B, int32_t H, int32_t topk, const int32_t* topk_idx, int32_t radius,
+                                    int32_t prev_dilation, int32_t projection, int32_t* const* row_ptrs,
+                                    int32_t* const* col_idxs, const int64_t* capacities, int32_t* const* orders,
+                                    hipStream_t stream) {
+  return map_steps(g, S, n_steps, ks, B, H, topk, topk_idx, radius, prev_dilation, projection, row_ptrs, col_idxs,
+                   capacities, orders, true, stream);
 }
 
 int sparvar_block_sparse_attn_fwd(const sparvar_geometry_t* g, int32_t k, int32_t B, int32_t H,

@@ -10,6 +10,8 @@
 //   (the largest possible row) and end with -1 padding, so no prefix sum and a
 //   single launch build them.
 // schedule_kernel (optional): the rows' longest-first stable order.
+#include <mutex>
+
 #include "device_common.h"
 #include "launch.h"
 #include "sparvar.h"
@@ -303,7 +305,8 @@ hipError_t launch_map_order(const GeoTable& G, int32_t BH, int32_t topk, int n_s
     const int32_t rows = BH * tiles_of(G, k);
     o.order = orders ? orders[i] : nullptr;
     const int32_t per_sel = steps[i].cover > 0 ? steps[i].cover : 1;
-    o.counts = steps[i].col_idx + (int64_t)rows * (steps[i].max_local + topk * per_sel);  // row lengths after the slots
+    // row lengths: after the row slots, or where the step's counts pointer says
+    o.counts = steps[i].counts ? steps[i].counts : steps[i].col_idx + (int64_t)rows * (steps[i].max_local + topk * per_sel);
     o.n_items = o.order ? f.n_items : 0;
     o.per = (o.n_items + 7) / 8;
     o.G_k = tiles_of(G, k);
@@ -346,7 +349,7 @@ hipError_t launch_map_index(const GeoTable& G, int S, int32_t BH, int32_t topk, 
     m.rows = BH * m.G_k;
     m.cover = a.cover;
     m.max_cand = a.max_local + topk * (a.cover > 0 ? a.cover : 1);
-    m.counts = a.col_idx + (int64_t)m.rows * m.max_cand;  // past the last row slot
+    m.counts = a.counts ? a.counts : a.col_idx + (int64_t)m.rows * m.max_cand;  // default: past the last row slot
     m.status = a.status;
     m.block0 = blocks;
     blocks += (m.rows + kMapWaves - 1) / kMapWaves;
@@ -361,6 +364,36 @@ hipError_t launch_map_index(const GeoTable& G, int S, int32_t BH, int32_t topk, 
   hipLaunchKernelGGL(schedule_kernel, dim3(grid), dim3(kMapWaves * 64), 0, stream, io.st[0].counts, io.st[0].rows,
                      schedule);
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- fixed scratch
+// Row lengths of the allocation-free mapping call: a fixed array in device
+// memory, one copy per device, held until the process ends. In host code the
+// array's name only stands for it; kernels get its device address, looked up
+// once per device.
+static __device__ __align__(256) int32_t scratch[kNoAllocMaxRows];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+int32_t* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t noalloc_row_lengths(int32_t** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = static_cast<int32_t*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace sparvar

@@ -5,6 +5,7 @@
 #include <stdint.h>
 
 #include "geometry.h"
+#include "sparvar.h"
 
 namespace sparvar {
 
@@ -162,7 +163,12 @@ struct MapStepArgs {
   int32_t *row_ptr, *col_idx;
   int32_t* status;  // nullable: set to SPARVAR_ERR_CAPACITY when a supplied local row is cut to max_local
   int32_t cover = 0;  // 0: point projection; else covering, with boxes of at most `cover` tiles
+  int32_t* counts = nullptr;  // row lengths; nullptr: after the last row slot of col_idx
 };
+// Rows whose lengths the allocation-free mapping call can hold (its fixed scratch).
+constexpr int32_t kNoAllocMaxRows = SPARVAR_NOALLOC_MAX_ROWS;
+// Device address of this device's fixed row-length scratch (looked up on first use).
+hipError_t noalloc_row_lengths(int32_t** out);
 constexpr int kMaxMapSteps = 8;
 // Rows of every listed step in one launch; the schedule (single step only) is
 // the longest-first order of that step's rows.

@@ -20,6 +20,7 @@ LIB_PATH = os.environ.get("SPARVAR_LIBRARY") or os.path.join(_HERE, "libsparvar.
 OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_CAPACITY, ERR_HIP = 0, -1, -2, -3, -4
 BF16, F32 = 0, 1
 MAX_SCALES = 32
+NOALLOC_MAX_ROWS = 1 << 20  # SPARVAR_NOALLOC_MAX_ROWS
 
 EXPORTS = [
     "sparvar_scale_info",
@@ -32,6 +33,7 @@ EXPORTS = [
     "sparvar_cs4a_map_tokens",
     "sparvar_cs4a_attn_fwd",
     "sparvar_map_index_steps",
+    "sparvar_map_index_steps_noalloc",
     "sparvar_kv_compact",
     "sparvar_csla_row_stride",
     "sparvar_csla_block_rows",
@@ -107,6 +109,8 @@ def load_library(path: str = LIB_PATH):
         "sparvar_cs4a_row_stride": (i32, [G, i32]),
         "sparvar_map_index_steps": (ctypes.c_int, [G, i32, i32, vp, i32, i32, i32, vp, i32, i32, i32, vp, vp, vp,
                                                    vp, vp]),
+        "sparvar_map_index_steps_noalloc": (ctypes.c_int, [G, i32, i32, vp, i32, i32, i32, vp, i32, i32, i32, vp, vp,
+                                                           vp, vp, vp]),
         "sparvar_kv_compact": (ctypes.c_int, [G, i32, vp, i32, i32, i32, ctypes.c_int, vp, vp, i64, vp, vp, i64, vp]),
         "sparvar_csla_row_stride": (i32, [G, i32, i32]),
         "sparvar_csla_block_rows": (ctypes.c_int, [G, i32, vp, i32, vp, i32, vp]),
@@ -410,9 +414,11 @@ def sparvar_map_index(geom, S, k, B, H, topk, topk_idx, local_row_ptr, local_col
 
 
 def sparvar_map_index_steps(geom, S, ks, B, H, topk, topk_idx, radius, row_ptrs, col_idxs, prev_dilation=0,
-                            orders=None, projection=PROJECT_POINT, stream=None):
+                            orders=None, projection=PROJECT_POINT, stream=None, noalloc=False):
     """The rows of several target scales in one launch (local rows generated); with orders (one int32 tensor of
-    B*H*G_k entries, or None, per step) also the attention launch order of each step."""
+    B*H*G_k entries, or None, per step) also the attention launch order of each step. noalloc=True calls
+    sparvar_map_index_steps_noalloc (row lengths in the library's fixed scratch; col_idxs need only the row
+    slots)."""
     n = len(ks)
     if not (len(row_ptrs) == len(col_idxs) == n):
         raise SparvarError(ERR_INVALID, "one row_ptr and col_idx per step is required")
@@ -426,12 +432,11 @@ def sparvar_map_index_steps(geom, S, ks, B, H, topk, topk_idx, radius, row_ptrs,
         if len(orders) != n:
             raise SparvarError(ERR_INVALID, "one order (or None) per step is required")
         ord_arr = (ctypes.c_void_p * max(n, 1))(*[(t.data_ptr() if t is not None else None) for t in orders])
-    _check(load_library().sparvar_map_index_steps(geom.ref, S, n, ctypes.cast(k_arr, vp), B, H, topk,
-                                                  _ptr(topk_idx), radius, prev_dilation, PROJECTIONS[projection],
-                                                  ctypes.cast(rp_arr, vp),
-                                                  ctypes.cast(ci_arr, vp), ctypes.cast(cap_arr, vp),
-                                                  ctypes.cast(ord_arr, vp) if ord_arr is not None else None,
-                                                  _stream(stream)))
+    lib = load_library()
+    fn = lib.sparvar_map_index_steps_noalloc if noalloc else lib.sparvar_map_index_steps
+    _check(fn(geom.ref, S, n, ctypes.cast(k_arr, vp), B, H, topk, _ptr(topk_idx), radius, prev_dilation,
+              PROJECTIONS[projection], ctypes.cast(rp_arr, vp), ctypes.cast(ci_arr, vp), ctypes.cast(cap_arr, vp),
+              ctypes.cast(ord_arr, vp) if ord_arr is not None else None, _stream(stream)))
 
 
 def sparvar_block_sparse_attn_fwd(geom, k, q_k, k_lek, v_lek, o, row_ptr, col_idx, lse=None, schedule=None,

@@ -328,3 +328,31 @@ def test_launch_option_names_follow_the_header():
     names = re.findall(r"SPARVAR_OPT_(\w+)", body)
     assert names[-1] == "COUNT" and names[0] == "SWIZZLE"
     assert names[:-1] == sv.LAUNCH_OPTIONS
+
+
+def test_noalloc_mapping_validation_before_launch():
+    # the allocation-free mapping call: capacities need only the row slots, and the
+    # steps' rows together must fit the fixed scratch of SPARVAR_NOALLOC_MAX_ROWS
+    lib = sv.load_library()
+    vp = ctypes.c_void_p
+    fake = 1 << 20
+    g = sv.Geometry(INF, INF, 8, 4)
+
+    def call(B, H, cap):
+        k_arr = (ctypes.c_int32 * 1)(13)
+        p_arr = (ctypes.c_void_p * 1)(fake)
+        c_arr = (ctypes.c_int64 * 1)(cap)
+        return lib.sparvar_map_index_steps_noalloc(g.ref, 10, 1, ctypes.cast(k_arr, vp), B, H, 8, vp(fake), 1, 0, 0,
+                                                   ctypes.cast(p_arr, vp), ctypes.cast(p_arr, vp),
+                                                   ctypes.cast(c_arr, vp), None, None)
+    H = sv.NOALLOC_MAX_ROWS // 64 + 1  # 64 tiles per plane at 64x64: one plane past the scratch
+    rows = H * 64
+    slots = sv.sparvar_map_index_capacity(g, 10, 13, 1, H, 8, 1) - rows
+    assert call(1, H, slots) == sv.ERR_CAPACITY
+    assert b"fixed scratch" in lib.sparvar_last_error()
+    rows = 2 * 16 * 64
+    slots = sv.sparvar_map_index_capacity(g, 10, 13, 2, 16, 8, 1) - rows
+    assert call(2, 16, slots - 1) == sv.ERR_CAPACITY           # the row slots are still required
+    assert b"capacity" in lib.sparvar_last_error()
+    with open(os.path.join(ROOT, "include", "sparvar.h")) as f:
+        assert f"#define SPARVAR_NOALLOC_MAX_ROWS (1 << {sv.NOALLOC_MAX_ROWS.bit_length() - 1})" in f.read()
