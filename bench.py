@@ -47,6 +47,9 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=200,
                     help="untimed steps first; about 70 ms of work, which brings the clocks up to speed")
+    ap.add_argument("--ramp-seconds", type=float, default=0.5,
+                    help="untimed whole steps for this long before the warm-up steps: the GPU reaches its "
+                         "steady clock after about 0.25 s of sustained work (0 = none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--sets", type=int, default=N_SETS)
@@ -566,6 +569,17 @@ def main():
             if ev is not None:
                 ev[3 + j].record(stream)
 
+    # clock ramp: whole steps for a fixed time, so that the warm-up and timed steps
+    # run at the steady clock (after 5 steps a layer takes about 18% longer than
+    # after 0.25 s of sustained work); nothing it computes is reused
+    t_ramp = time.perf_counter()
+    n_ramp = 0
+    while time.perf_counter() - t_ramp < args.ramp_seconds:
+        for _ in range(10):
+            one_step(n_ramp)
+            n_ramp += 1
+        torch.cuda.synchronize()
+    ramp_s = time.perf_counter() - t_ramp
     for i in range(args.warmup):
         one_step(i)
     torch.cuda.synchronize()
@@ -713,6 +727,7 @@ def main():
                    "block": "8x8 tokens", "topk": CFG["topk"], "window_radius": CFG["radius"],
                    "sink_scales": CFG["n_sink"], "kv_tokens_last_step": info[13]["n_tokens_le"]},
         "value_is": "algorithmic TFLOP/s of the block-sparse attention at the 64x64 step, timed inside the step",
+        "clock_ramp": {"seconds": ramp_s, "steps": n_ramp},
         "ms_per_layer": ms_step,
         "layer_tflops": step_flops / ms_step / 1e9,
         "ms_per_step_spread": {"median": float(np.median(step_ms)), "p10": float(np.percentile(step_ms, 10)),
