@@ -216,6 +216,7 @@ def sweep(args, dev, only=None):
 
     d, nf, ns = CFG["d"], CFG["n_freq"], CFG["n_sink"]
     cache = {}
+    ramp_left = args.ramp_seconds  # the first workload also brings the clocks up
     for st in SWEEP:
         if only is not None and only not in st["name"]:
             continue
@@ -255,6 +256,14 @@ def sweep(args, dev, only=None):
         for i in range(5):
             one(i)
         torch.cuda.synchronize()
+        t_ramp, i = time.perf_counter(), 5
+        while time.perf_counter() - t_ramp < ramp_left:
+            one(i)
+            i += 1
+            if i % 10 == 0:
+                torch.cuda.synchronize()
+        torch.cuda.synchronize()
+        ramp_left = 0.0
         n = 20
         evs = [[torch.cuda.Event(enable_timing=True) for _ in range(n_ev)] for _ in range(n)]
         for i in range(n):
