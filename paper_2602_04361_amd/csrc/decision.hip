@@ -9,7 +9,8 @@
 // tile-row band (<= 32 keys) at a time through their own two LDS stages, with
 // the attention core of attn_chunk.h, and keep for every query the probability
 // mass of each block relative to the running max (rescaled with the
-// accumulator whenever the max moves). After the walk the splits are merged in
+// accumulator whenever the max moves): the current block's in a register, each
+// finished block's in LDS. After the walk the splits are merged in
 // LDS (max, sum, output), and a block's score is sum over the tile's queries of
 // its mass divided by that query's softmax sum: exactly the sum of the
 // normalised probabilities. Top-k follows in the same workgroup: a block is
@@ -143,6 +144,7 @@ __global__ __launch_bounds__(WPT * KS * 64) void decision_kernel(DecisionIO io) 
     bool last = false;
     bool have = walk.next(cur, blk, last);
     if (have) issue(cur, s0);
+    float cur_mass = 0.f;  // the current block's mass, stored when its last chunk is done
     auto step = [&](auto st_c) {
       constexpr int ST = decltype(st_c)::value;
       char* const stg = ST == 0 ? s0 : s1;
@@ -167,17 +169,22 @@ __global__ __launch_bounds__(WPT * KS * 64) void decision_kernel(DecisionIO io) 
 #pragma unroll
           for (int i = 0; i < D / 32; ++i) acc[i] *= alpha;
           if (half == 0)
-            for (int32_t u = 0; u <= blk - v0; ++u) my_mass[u] *= alpha;
+            for (int32_t u = 0; u < blk - v0; ++u) my_mass[u] *= alpha;
+          cur_mass *= alpha;
           m_run = m_new;
         }
         const float p = exp_pack<KC>(sc, sl2, m_run, pf);
         l_run += p;
         pv_chunk<D, KC>(stg, fo, pf, acc);
-        const float qsum = sum_halves(p);
-        if (half == 0) my_mass[blk - v0] += qsum;
+        cur_mass += sum_halves(p);
+        if (last) {
+          if (half == 0) my_mass[blk - v0] = cur_mass;
+          cur_mass = 0.f;
+        }
       }
       cur = nxt;
       blk = nblk;
+      last = nlast;
       have = have_n;
     };
     for (int32_t s = 0; s < io.steps; s += 2) {
