@@ -27,7 +27,9 @@
  *    scale-major and row-major over tiles inside a scale. Query tiles of
  *    scale k use the same tiling ("query blocks" of the paper).
  *  - Every pointer except the geometry is device memory owned by the caller.
- *    The library allocates no device memory and never synchronises: work is
+ *    The library allocates no device memory (the allocation-free mapping call
+ *    uses a fixed array that is part of the library's device code, one per
+ *    device) and never synchronises: work is
  *    enqueued on `stream` (NULL = the default stream) and results are valid
  *    once the caller has synchronised that stream.
  *  - Process-wide state: the message of the last failure (one per calling
